@@ -1,0 +1,86 @@
+/*
+ * CATS CPU oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, sequential CPU implementation of what the CATS gated-MLP
+ * computes (Lee et al., "CATS: Contextually-Aware Thresholding for Sparsity
+ * in Large Language Models", COLM 2024).  Only the test suite, the smoke
+ * check and the benchmark's CPU-baseline leg may load this library; the
+ * product path (libcats) never links or calls it, and the two share no
+ * code, header or helper.
+ *
+ * Precision: the paper runs all experiments in FP32 (Section 4, setup), so
+ * the default build accumulates in float with a strictly ascending index
+ * order and no fused multiply-add (-O2 -ffp-contract=off, no fast-math).
+ * Building with -DORACLE_F64 gives the same code in double, which bounds
+ * the float build's own rounding.
+ *
+ * Layouts follow the paper's notation (Section 2, Eq. 1):
+ *   x       [B x d]   row-major
+ *   w_gate  [d x m]   row-major (math layout, element (i,j) at i*m + j)
+ *   w_up    [d x m]   row-major
+ *   w_down  [m x d]   row-major (element (j,k) at j*d + k)
+ * All pointers are host pointers owned by the caller.
+ */
+#ifndef CATS_ORACLE_H
+#define CATS_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Name of the accumulation type of this build: "f32" or "f64". */
+const char* oracle_precision(void);
+
+/* SiLU(z) = z / (1 + exp(-z)) (Eq. 2), evaluated in the build's precision. */
+double oracle_silu(double z);
+
+/* The gated MLP with the CATS activation (Eq. 1 with Eq. 5, and the
+ * "MLP using CATS" algorithm of Section 3.3).  For every row b:
+ *   g_j = sum_i x_bi Wg[i,j],  u_j = sum_i x_bi Wu[i,j]   (ascending i)
+ *   v_j = SiLU(g_j)
+ *   neuron j is active when |v_j| >= t   (written !(|v_j| < t); Eq. 4)
+ *   s_k = sum over active j, ascending, of (v_j u_j) Wd[j,k]   (from +0)
+ *   y_bk = residual_bk + s_k     (residual may be NULL: y = s)
+ * dense != 0 keeps every neuron (plain Eq. 1).  t = 0 keeps every neuron as
+ * well, so it reproduces dense bit for bit.
+ * Optional outputs (NULL to skip), per row b, in ascending neuron order:
+ *   active_idx[b*m + q], active_cnt[b], v_all[b*m + j] (every j),
+ *   h_act[b*m + q] = v_j u_j of the q-th active neuron.
+ * Returns 0, or -1 on a bad argument. */
+int oracle_cats_mlp(const float* x, int32_t B, int32_t d, int32_t m,
+                    const float* w_gate, const float* w_up, const float* w_down,
+                    double t, int32_t dense, const float* residual,
+                    double* y, int32_t* active_idx, int32_t* active_cnt,
+                    double* v_all, double* h_act);
+
+/* RMSNorm with unit gain: out_bi = x_bi / sqrt(mean_i(x_bi^2) + eps),
+ * the sum of squares taken in ascending i. */
+int oracle_rmsnorm(const float* x, int32_t B, int32_t d, double eps, double* out);
+
+/* Calibration activations (Section 3.1): a[n*m + j] = |SiLU(x_n . Wg[:,j])|
+ * for N calibration vectors. */
+int oracle_calib_acts(const float* X, int32_t N, int32_t d, int32_t m,
+                      const float* w_gate, double* acts);
+
+/* The same activations for an explicit list of (n, j) pairs
+ * (pairs[2q] = n, pairs[2q+1] = j), for sampled checks at full size. */
+int oracle_calib_acts_at(const float* X, int32_t N, int32_t d, int32_t m,
+                         const float* w_gate, const int64_t* pairs,
+                         int64_t npairs, double* out);
+
+/* Rank of the cutoff order statistic for sparsity k over n values
+ * (Eq. 3 on the empirical CDF): r = ceil(k*n - 1e-6) clamped to [1, n].
+ * Returns 0 when k == 0 (the cutoff is then t = 0).  -1 on bad input. */
+int64_t oracle_cutoff_rank(int64_t n, double k);
+
+/* Cutoff threshold t = min{t' : F(t') >= k} (Eq. 3), F the empirical CDF of
+ * |a| over the n given values: the r-th smallest |a| (1-indexed), found by
+ * sorting a copy.  k == 0 gives 0.  Returns 0 and writes *t, or -1. */
+int oracle_threshold(const double* a, int64_t n, double k, double* t);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
