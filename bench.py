@@ -1,0 +1,233 @@
+#!/usr/bin/env python3
+"""Benchmark: CATS MLP us/layer and effective HBM GB/s at batch 1.
+
+Workload: one Llama2-7B-shaped MLP block (d=4096, m=11008, bf16 weights,
+fp32 arithmetic), synthetic seeded weights and decode vectors (1% of the
+input channels scaled x20), cutoffs calibrated on 2048 vectors at
+sparsities 0.5, 0.7 and 0.9.  One step = one CATS forward of one token at
+each of the three sparsities.  Eight copies of the weights rotate between
+calls so no call finds its weights in the 256 MB MALL.
+
+value = sum of required bytes / timed wall time, where a call's required
+bytes are s_w*d*(m + 2*n_act) + 8*d + 8*n_act with n_act the measured active
+count of that token (full W_gate, plus the active rows of W_up and W_down).
+
+Also reported: per-sparsity us and GB/s, the dense kernel, the roofline of
+the dominant kernel (HIP events on its launch stream over an identical
+timed region), and the CPU oracle on a bounded sample (baseline only).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "CATS MLP µs/layer + effective HBM GB/s (batch 1) at 50/70/90% sparsity"
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=80)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="C2", choices=["C2", "C3"])
+    ap.add_argument("--sparsities", default="0.5,0.7,0.9")
+    ap.add_argument("--rotate", type=int, default=8)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true", help="only the timed region (for profilers)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the CATS MLP hot path has no multi-GPU "
+              "path in this build (see DESIGN.md for how it would shard); run with --gpus 1",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2404_08763_amd as P
+    from paper_2404_08763_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    cfg = W.CONFIGS[args.config]
+    ks = [float(s) for s in args.sparsities.split(",")]
+    sw = 2 if cfg.wdtype == torch.bfloat16 else 4
+    d, m = cfg.d, cfg.m
+    R = max(1, args.rotate)
+
+    log(f"[bench] generating {cfg.name} weights d={d} m={m}")
+    wg, wu, wd = W.weights(d, m, cfg.wdtype)
+    base = P.layer_from_math(wg.to(dev), wu.to(dev), wd.to(dev))
+    layers = [base] + [P.Layer(base.w_gate_t.clone(), base.w_up_t.clone(), base.w_down.clone())
+                       for _ in range(R - 1)]
+    xcal = W.calib_vectors(cfg).to(dev)
+    xs = W.decode_vectors(cfg).to(dev)
+    ntok = xs.shape[0]
+    torch.cuda.synchronize()
+
+    # cutoffs (Eq. 3) on the device, timed
+    wsc = P.workspace(d, m, 1, xcal.shape[0] * m, device=dev)
+    thr = {}
+    t0 = time.perf_counter()
+    for k in ks:
+        thr[k] = P.calibrate_threshold(base, xcal, k, ws=wsc)
+    calib_ms = (time.perf_counter() - t0) * 1e3 / len(ks)
+    del wsc
+    log(f"[bench] thresholds {thr} ({calib_ms:.1f} ms per calibration)")
+
+    ws = P.workspace(d, m, 1, device=dev)
+    y = torch.empty((1, d), dtype=torch.float32, device=dev)
+
+    # measured active counts of every (token, k); deterministic, so the timed
+    # calls below activate exactly these neurons
+    nact = {k: np.zeros(ntok, np.int64) for k in ks}
+    for k in ks:
+        for i in range(ntok):
+            _, aux = P.mlp_forward(base, xs[i : i + 1], thr[k], out=y, ws=ws, aux=True)
+            nact[k][i] = int(aux["cnt"][0])
+    torch.cuda.synchronize()
+
+    def req_bytes(n):
+        return sw * d * (m + 2 * n) + 8 * d + 8 * n
+
+    def k1_bytes(n):  # what the fused kernel itself must move: weights + x
+        return sw * d * (m + 2 * n) + 4 * d
+
+    # raw C-ABI calls with prebuilt arguments: keeps host overhead far below
+    # the device time of a call
+    L = P.raw()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    xptr = [ctypes.c_void_p(xs[i : i + 1].data_ptr()) for i in range(ntok)]
+    yptr = ctypes.c_void_p(y.data_ptr())
+    wsp, wsn = ctypes.c_void_p(ws.data_ptr()), ws.numel()
+    fwd, dense = L.cats_mlp_forward, L.cats_mlp_dense
+
+    def call_cats(li, i, k):
+        st = fwd(layers[li].c, xptr[i], 1, ctypes.c_float(thr[k]), None, yptr, None, wsp, wsn, stream)
+        if st != 0:
+            raise P.CatsError(st, L.cats_last_error().decode())
+
+    def call_dense(li, i):
+        st = dense(layers[li].c, xptr[i], 1, None, yptr, wsp, wsn, stream)
+        if st != 0:
+            raise P.CatsError(st, L.cats_last_error().decode())
+
+    def step(s):
+        for j, k in enumerate(ks):
+            call_cats((s * len(ks) + j) % R, s % ntok, k)
+
+    def timed(fn, n_warm, n_iter):
+        for s in range(n_warm):
+            fn(s)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for s in range(n_iter):
+            fn(n_warm + s)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    K, Wm = args.steps, args.warmup
+    # ---- the timed region of the contract
+    ms_total = timed(step, Wm, K)
+    bytes_total = sum(req_bytes(int(nact[k][(Wm + s) % ntok])) for s in range(K) for k in ks)
+    value = bytes_total / (ms_total * 1e-3) / 1e9
+    ms_per_step = ms_total / K
+    log(f"[bench] {K} steps in {ms_total:.3f} ms -> {value:.1f} GB/s")
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": K,
+        "warmup": Wm, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name}: single Llama2-7B-shaped gated-MLP layer" if cfg.name == "C2"
+            else f"{cfg.name}: single Mistral-7B-shaped gated-MLP layer",
+            "d": d, "m": m, "weights": "bf16" if sw == 2 else "f32", "batch": 1,
+            "sparsities": ks, "step": "one CATS forward per sparsity, one token each",
+            "weight_copies_rotated": R, "decode_vectors": ntok,
+        },
+    }
+
+    if not args.no_extras:
+        per_k = {}
+        for k in ks:
+            msk = timed(lambda s, k=k: call_cats(s % R, s % ntok, k), Wm, K)
+            nb = sum(req_bytes(int(nact[k][(Wm + s) % ntok])) for s in range(K))
+            per_k[k] = (msk * 1e3 / K, nb / (msk * 1e-3) / 1e9)
+        msd = timed(lambda s: call_dense(s % R, s % ntok), Wm, K)
+        dense_us = msd * 1e3 / K
+        dense_gbps = req_bytes(m) / (dense_us * 1e-6) / 1e9
+        out["us_per_layer"] = {str(k): round(per_k[k][0], 3) for k in ks}
+        out["gbps"] = {str(k): round(per_k[k][1], 1) for k in ks}
+        out["frac_of_hbm_peak"] = {str(k): round(per_k[k][1] / HBM_PEAK_GBPS, 4) for k in ks}
+        out["dense_us_per_layer"] = round(dense_us, 3)
+        out["dense_gbps"] = round(dense_gbps, 1)
+        out["speedup_vs_dense"] = {str(k): round(dense_us / per_k[k][0], 3) for k in ks}
+        out["n_act_mean"] = {str(k): round(float(nact[k].mean()), 1) for k in ks}
+        out["thresholds"] = {str(k): thr[k] for k in ks}
+        out["calib_ms"] = round(calib_ms, 2)
+
+        # ---- roofline of the dominant kernel: HIP events recorded by libcats
+        # on the launch stream around every kernel, over an identical region
+        P.timer_reset()
+        P.timer_enable(True)
+        ms_timer = timed(step, 0, K)
+        P.timer_enable(False)
+        kt = P.timer_read()
+        name = "mlp_fused_cats"
+        n_launch, ms_k1 = kt.get(name, (0, 0.0))
+        k1_total = sum(k1_bytes(int(nact[k][s % ntok])) for s in range(K) for k in ks)
+        avg_us = ms_k1 * 1e3 / max(1, n_launch)
+        achieved = (k1_total / max(1, n_launch)) / (avg_us * 1e-6) / 1e9
+        out["roofline"] = {
+            "kernel": "k_mlp_fused (CATS)", "bound": "hbm", "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": None, "avg_launch_us": round(avg_us, 3), "launches": n_launch,
+            "bytes_per_launch": int(k1_total / max(1, n_launch)),
+        }
+        out["kernel_avg_us"] = {n: round(v[1] * 1e3 / max(1, v[0]), 3) for n, v in kt.items()}
+        out["timed_region_with_kernel_events_ms_per_step"] = round(ms_timer / K, 5)
+
+    if not args.no_cpu_baseline:
+        import oracle
+
+        O = oracle.load("f32")
+        hw = [t.float().numpy() for t in (wg, wu, wd)]
+        xh = xs.cpu().numpy()
+        k = ks[0]
+        tsum, bsum, n = 0.0, 0, 0
+        while n < 1 or (tsum < args.cpu_seconds and n < ntok):
+            t1 = time.perf_counter()
+            r = O.cats_mlp(xh[n : n + 1], *hw, t=thr[k])
+            tsum += time.perf_counter() - t1
+            bsum += req_bytes(int(r["cnt"][0]))
+            n += 1
+        out["cpu_baseline"] = {
+            "value": round(bsum / tsum / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} tokens of the {cfg.name} layer at k={k}, fp32 oracle, 1 thread "
+                      f"({tsum * 1e3 / n:.1f} ms per token)",
+        }
+
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,190 @@
+/*
+ * libcats -- CATS (Contextually-Aware Thresholding for Sparsity) gated-MLP
+ * hot path for AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow Lee et al., "CATS: Contextually-Aware Thresholding
+ * for Sparsity in Large Language Models" (COLM 2024):
+ *   Section 2, Eq. 1   Gated-MLP(x) = (SiLU(x W_gate) * (x W_up)) W_down,
+ *                      x in R^{b x d}, W_gate, W_up in R^{d x m},
+ *                      W_down in R^{m x d}
+ *   Section 2, Eq. 2   SiLU(z) = z / (1 + e^{-z})
+ *   Section 3.1, Eq. 3 cutoff t = min{t' : F(t') >= k}, F the empirical CDF
+ *                      of the absolute gate activations of one MLP block
+ *   Section 3.2, Eq. 4-5  CATS_t keeps an activation when |.| >= t
+ *   Section 3.3 and Appendix D  kernel algorithms "MLP using CATS"
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Plain C ABI.  Every pointer argument is caller-owned; the library never
+ *    frees or keeps a pointer after returning.  "dev" marks device memory,
+ *    "host" host memory.  `stream` is a hipStream_t (NULL = the default
+ *    stream of the current device); every device pointer must belong to the
+ *    current device.
+ *  - The forward, dense, pack and rmsnorm calls only enqueue work on
+ *    `stream` (no host synchronisation, no allocation).  Outputs are valid
+ *    once the stream reaches that point.  The two calibration calls
+ *    synchronise `stream` because they return t on the host.
+ *  - Arguments are validated on the host before any HIP call; a rejected
+ *    call returns its status and touches nothing.  HIP failures return
+ *    CATS_ERR_HIP.  cats_last_error() gives a message for the last failure
+ *    on the calling thread.  No call aborts or throws.
+ *  - Scratch memory comes from a caller-provided workspace `ws` of
+ *    `ws_bytes` bytes (256-byte aligned, device), sized with
+ *    cats_workspace_bytes().  Calls that run concurrently need separate
+ *    workspaces.
+ *  - x, y, residual, thresholds and calibration inputs are fp32.  Weights
+ *    are CATS_F32 or CATS_BF16; all arithmetic accumulates in fp32.
+ *  - Weight layout is neuron-major: W_gate^T and W_up^T are stored [m x d]
+ *    (row j holds neuron j's d input weights contiguously, the paper's
+ *    "column-major W_up"), W_down is [m x d] row-major as in Eq. 1.  Use
+ *    cats_pack_weights to produce W^T from the math layout [d x m].
+ */
+#ifndef CATS_H
+#define CATS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CATS_VERSION 1
+
+typedef enum {
+  CATS_OK = 0,
+  CATS_ERR_NULL = 1,          /* a required pointer is NULL */
+  CATS_ERR_SHAPE = 2,         /* d, m, B or N out of the supported range */
+  CATS_ERR_RANGE = 3,         /* sparsity or t outside its domain */
+  CATS_ERR_DTYPE = 4,         /* unknown weight dtype */
+  CATS_ERR_ALIGN = 5,         /* a pointer misses its required alignment */
+  CATS_ERR_WORKSPACE = 6,     /* workspace NULL or too small */
+  CATS_ERR_HIP = 7,           /* a HIP runtime call failed */
+  CATS_ERR_UNIMPLEMENTED = 8  /* combination not supported by this build */
+} cats_status;
+
+typedef enum { CATS_F32 = 0, CATS_BF16 = 1 } cats_dtype;
+
+/* Supported sizes.  d must be a positive multiple of 8 (16-byte vector
+ * loads of bf16 rows); 1 <= m <= CATS_MAX_M; batch rows 1..CATS_MAX_BATCH. */
+#define CATS_MAX_D_BF16 8192
+#define CATS_MAX_M 65536
+#define CATS_MAX_D_F32 4096
+#define CATS_MAX_BATCH 16
+/* Each weight matrix (m * d elements) is addressed with 32-bit offsets and
+ * may span at most 1 GiB. */
+#define CATS_MAX_MATRIX_BYTES (1ull << 30)
+
+/* One gated-MLP block (Eq. 1) in neuron-major layout.  Plain data: the
+ * struct and the weights stay owned by the caller. */
+typedef struct {
+  int32_t d;              /* hidden size */
+  int32_t m;              /* intermediate size (number of neurons) */
+  int32_t wdtype;         /* cats_dtype of all three matrices */
+  const void* w_gate_t;   /* dev [m x d], row j = W_gate[:, j] */
+  const void* w_up_t;     /* dev [m x d], row j = W_up[:, j] */
+  const void* w_down;     /* dev [m x d], row j = W_down[j, :] */
+} cats_layer;
+
+/* Optional per-row outputs of cats_mlp_forward; any member may be NULL.
+ * For batch row b, in ascending neuron order:
+ *   active_idx[b*m + q]  index of the q-th neuron kept by CATS_t (Eq. 5)
+ *   active_cnt[b]        number of kept neurons
+ *   active_v[b*m + q]    its activation v = SiLU(x W_gate[:, j]) (Eq. 2)
+ *   active_h[b*m + q]    v * (x W_up[:, j]), the x1 of the CATS kernel
+ *                        algorithm (Section 3.3), before W_down
+ * Entries past active_cnt[b] are left untouched.  All dev, int32 / fp32. */
+typedef struct {
+  int32_t* active_idx;
+  int32_t* active_cnt;
+  float* active_v;
+  float* active_h;
+} cats_forward_aux;
+
+/* Library version (CATS_VERSION). */
+int32_t cats_version(void);
+
+/* Static description of a status code; never NULL. */
+const char* cats_status_string(cats_status s);
+
+/* Message for the last failed call on this thread ("" if none). */
+const char* cats_last_error(void);
+
+/* Workspace bytes needed by any call on a block of size d x m with up to
+ * `max_batch` rows per forward/dense call and up to `max_calib_values`
+ * calibration activations (N * m) per calibration call (0 if calibration
+ * is not used).  Pure host arithmetic, no HIP call.  Returns 0 for
+ * arguments outside the supported range. */
+size_t cats_workspace_bytes(int32_t d, int32_t m, int32_t max_batch, int64_t max_calib_values);
+
+/* Transpose a row-major [rows x cols] matrix into [cols x rows]
+ * (w_t[c*rows + r] = w[r*cols + c]), bit for bit.  Used to turn the math
+ * layout W_gate, W_up [d x m] of Eq. 1 into the neuron-major [m x d]
+ * the kernels stream (Section 3.3 stores W_up this way so that a masked
+ * neuron's weights are one contiguous row).  dev w, dev w_t, no overlap. */
+cats_status cats_pack_weights(const void* w, void* w_t, int32_t rows, int32_t cols,
+                              int32_t dtype, void* stream);
+
+/* Calibration activations (Section 3.1): for N vectors x_n (dev [N x d],
+ * fp32) writes acts[n*m + j] = |SiLU(x_n . W_gate[:, j])| (dev [N x m]).
+ * Enqueue only. */
+cats_status cats_calib_activations(const cats_layer* layer, const float* x, int32_t N,
+                                   float* acts, void* stream);
+
+/* Cutoff threshold from activations (Eq. 3): with n values a (dev, fp32;
+ * the absolute value is taken inside) returns in *t_out (host) the r-th
+ * smallest |a|, r = ceil(k*n - 1e-6) clamped to [1, n], which is
+ * min{t' : F(t') >= k} for the empirical CDF F.  k = sparsity in [0, 1];
+ * k = 0 gives t = 0 without touching the device.  Selection is exact (a
+ * radix select on the fp32 bit patterns).  Synchronises `stream`. */
+cats_status cats_threshold_from_acts(const float* acts, int64_t n, double sparsity,
+                                     void* ws, size_t ws_bytes, void* stream, float* t_out);
+
+/* Per-block cutoff calibration (Section 3.1, Eq. 3): activations of the N
+ * calibration vectors (dev [N x d], fp32) through the gate, pooled over
+ * all N*m values, then cats_threshold_from_acts.  *t_out is host.
+ * Synchronises `stream`.  Needs max_calib_values >= N*m in the workspace. */
+cats_status cats_calibrate_threshold(const cats_layer* layer, const float* calib_x, int32_t N,
+                                     double sparsity, void* ws, size_t ws_bytes, void* stream,
+                                     float* t_out);
+
+/* CATS MLP forward (Eq. 1 with the CATS_t activation of Eq. 5; the
+ * "MLP using CATS" algorithm of Section 3.3):
+ *   v = SiLU(x W_gate); Mask = |v| >= t; x1 = (x W_up[Mask]) * v[Mask];
+ *   y = residual + x1 W_down[Mask]
+ * for B rows x (dev [B x d]); y (dev [B x d]); residual dev [B x d] or
+ * NULL.  t >= 0 (t = +inf masks everything, y = residual or 0); each row
+ * has its own Mask, and the rows of W_up / W_down read are the union of
+ * the rows' masks.  Only the active rows of W_up and W_down are read.
+ * aux may be NULL.  y must not alias x.  Enqueue only. */
+cats_status cats_mlp_forward(const cats_layer* layer, const float* x, int32_t B, float t,
+                             const float* residual, float* y, const cats_forward_aux* aux,
+                             void* ws, size_t ws_bytes, void* stream);
+
+/* Dense gated MLP (Eq. 1, every neuron kept): the comparison baseline
+ * ("Dense" of Section 4.3).  Same arguments and layouts as the forward. */
+cats_status cats_mlp_dense(const cats_layer* layer, const float* x, int32_t B,
+                           const float* residual, float* y, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/* RMSNorm with unit gain, xn = x / sqrt(mean(x^2) + eps), rows of d fp32
+ * (dev [B x d]); the normalisation in front of each MLP block of a
+ * decoder stack (the paper leaves norms out of its formulas, Appendix B).
+ * B >= 1, any d >= 1, eps >= 0.  Enqueue only. */
+cats_status cats_rmsnorm(const float* x, float* xn, int32_t B, int32_t d, float eps,
+                         void* stream);
+
+/* Per-kernel timing.  While enabled, every kernel the library launches is
+ * bracketed by HIP events recorded on its launch stream.  cats_timer_get
+ * waits for the pending events and returns, for kernel name i, the number
+ * of launches and their summed duration in ms.  Not for use under graph
+ * capture. */
+cats_status cats_timer_enable(int32_t on);
+cats_status cats_timer_reset(void);
+int32_t cats_timer_count(void);
+cats_status cats_timer_get(int32_t i, const char** name, int64_t* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CATS_H */

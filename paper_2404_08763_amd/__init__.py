@@ -1,0 +1,31 @@
+"""CATS gated-MLP hot path for AMD Instinct MI355X (gfx950).
+
+CATS (Contextually-Aware Thresholding for Sparsity, Lee et al., COLM 2024)
+wraps the SiLU of a gated MLP in a magnitude cutoff t calibrated per block
+(Eq. 3-5) and then reads only the W_up / W_down rows of the neurons that
+survive (Section 3.3).  The work runs in hand-written HIP kernels inside
+libcats.so behind a C ABI (include/cats.h); this package is its ctypes
+binding.  Build with ``python -m paper_2404_08763_amd.build``.
+"""
+from ._lib import (  # noqa: F401
+    CATS_BF16,
+    CATS_F32,
+    CatsError,
+    Layer,
+    calib_activations,
+    calibrate_threshold,
+    layer_from_math,
+    lib_path,
+    mlp_dense,
+    mlp_forward,
+    pack_weights,
+    raw,
+    rmsnorm,
+    threshold_from_acts,
+    timer_enable,
+    timer_read,
+    timer_reset,
+    version,
+    workspace,
+    workspace_bytes,
+)

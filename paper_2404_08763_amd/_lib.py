@@ -1,0 +1,311 @@
+"""ctypes binding of libcats (the C ABI declared in include/cats.h).
+
+Argument marshalling only: every function passes device pointers of torch
+tensors and the current HIP stream to the library, which does all the work
+in its own kernels.  torch supplies device memory and streams.  There is no
+fallback: if libcats.so is missing the import fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+# torch is imported first so that libcats binds to the HIP runtime torch
+# already loaded (both carry the soname libamdhip64.so.7); loading libcats
+# first would pull in a second runtime.
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcats.so")
+
+CATS_F32 = 0
+CATS_BF16 = 1
+STATUS_NAMES = {
+    0: "CATS_OK", 1: "CATS_ERR_NULL", 2: "CATS_ERR_SHAPE", 3: "CATS_ERR_RANGE",
+    4: "CATS_ERR_DTYPE", 5: "CATS_ERR_ALIGN", 6: "CATS_ERR_WORKSPACE", 7: "CATS_ERR_HIP",
+    8: "CATS_ERR_UNIMPLEMENTED",
+}
+
+
+class CatsError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class _Layer(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("m", ctypes.c_int32), ("wdtype", ctypes.c_int32),
+                ("w_gate_t", ctypes.c_void_p), ("w_up_t", ctypes.c_void_p),
+                ("w_down", ctypes.c_void_p)]
+
+
+class _Aux(ctypes.Structure):
+    _fields_ = [("active_idx", ctypes.c_void_p), ("active_cnt", ctypes.c_void_p),
+                ("active_v", ctypes.c_void_p), ("active_h", ctypes.c_void_p)]
+
+
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_i64 = ctypes.c_int64
+_sz = ctypes.c_size_t
+_f32 = ctypes.c_float
+_f64 = ctypes.c_double
+
+_SIGNATURES = {
+    "cats_version": ([], _i32),
+    "cats_status_string": ([_i32], ctypes.c_char_p),
+    "cats_last_error": ([], ctypes.c_char_p),
+    "cats_workspace_bytes": ([_i32, _i32, _i32, _i64], _sz),
+    "cats_pack_weights": ([_vp, _vp, _i32, _i32, _i32, _vp], _i32),
+    "cats_calib_activations": ([ctypes.POINTER(_Layer), _vp, _i32, _vp, _vp], _i32),
+    "cats_threshold_from_acts": ([_vp, _i64, _f64, _vp, _sz, _vp, ctypes.POINTER(_f32)], _i32),
+    "cats_calibrate_threshold": ([ctypes.POINTER(_Layer), _vp, _i32, _f64, _vp, _sz, _vp,
+                                  ctypes.POINTER(_f32)], _i32),
+    "cats_mlp_forward": ([ctypes.POINTER(_Layer), _vp, _i32, _f32, _vp, _vp, ctypes.POINTER(_Aux),
+                          _vp, _sz, _vp], _i32),
+    "cats_mlp_dense": ([ctypes.POINTER(_Layer), _vp, _i32, _vp, _vp, _vp, _sz, _vp], _i32),
+    "cats_rmsnorm": ([_vp, _vp, _i32, _i32, _f32, _vp], _i32),
+    "cats_timer_enable": ([_i32], _i32),
+    "cats_timer_reset": ([], _i32),
+    "cats_timer_count": ([], _i32),
+    "cats_timer_get": ([_i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(_i64),
+                        ctypes.POINTER(_f64)], _i32),
+}
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def raw() -> ctypes.CDLL:
+    """The loaded libcats handle (signatures set).  Raises if not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise ImportError(f"libcats.so is not built ({_LIB_PATH}); run "
+                              "`python -m paper_2404_08763_amd.build` first")
+        L = ctypes.CDLL(_LIB_PATH, mode=ctypes.RTLD_GLOBAL)
+        for name, (args, res) in _SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        msg = raw().cats_last_error().decode(errors="replace")
+        raise CatsError(status, msg)
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def _wdtype(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return CATS_BF16
+    if dt == torch.float32:
+        return CATS_F32
+    raise ValueError(f"unsupported weight dtype {dt}")
+
+
+@dataclass
+class Layer:
+    """One gated-MLP block in neuron-major layout (all [m, d] device tensors)."""
+    w_gate_t: torch.Tensor
+    w_up_t: torch.Tensor
+    w_down: torch.Tensor
+
+    def __post_init__(self):
+        m, d = self.w_gate_t.shape
+        for n, w in (("w_gate_t", self.w_gate_t), ("w_up_t", self.w_up_t), ("w_down", self.w_down)):
+            _dev(w, n, self.w_gate_t.dtype)
+            if tuple(w.shape) != (m, d):
+                raise ValueError(f"{n} has shape {tuple(w.shape)}, expected {(m, d)}")
+        self._c = _Layer(d, m, _wdtype(self.w_gate_t.dtype), self.w_gate_t.data_ptr(),
+                         self.w_up_t.data_ptr(), self.w_down.data_ptr())
+
+    @property
+    def d(self) -> int:
+        return int(self.w_gate_t.shape[1])
+
+    @property
+    def m(self) -> int:
+        return int(self.w_gate_t.shape[0])
+
+    @property
+    def c(self):
+        return ctypes.byref(self._c)
+
+
+def version() -> int:
+    return int(raw().cats_version())
+
+
+def workspace_bytes(d: int, m: int, max_batch: int = 1, max_calib_values: int = 0) -> int:
+    return int(raw().cats_workspace_bytes(d, m, max_batch, max_calib_values))
+
+
+def workspace(d: int, m: int, max_batch: int = 1, max_calib_values: int = 0, device="cuda") -> torch.Tensor:
+    """A device byte buffer of cats_workspace_bytes(...) bytes."""
+    n = workspace_bytes(d, m, max_batch, max_calib_values)
+    if n == 0:
+        raise ValueError("arguments outside the supported range")
+    ws = torch.empty(n, dtype=torch.uint8, device=device)
+    assert ws.data_ptr() % 256 == 0
+    return ws
+
+
+def pack_weights(w: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """[rows, cols] -> [cols, rows] transpose on the device (bit-exact)."""
+    _dev(w, "w")
+    rows, cols = w.shape
+    if out is None:
+        out = torch.empty((cols, rows), dtype=w.dtype, device=w.device)
+    _dev(out, "out", w.dtype)
+    _check(raw().cats_pack_weights(_ptr(w), _ptr(out), rows, cols, _wdtype(w.dtype), _stream()))
+    return out
+
+
+def layer_from_math(w_gate: torch.Tensor, w_up: torch.Tensor, w_down: torch.Tensor) -> Layer:
+    """Build a Layer from math-layout weights (W_gate, W_up [d, m]; W_down [m, d])."""
+    return Layer(pack_weights(w_gate), pack_weights(w_up), w_down.contiguous())
+
+
+def calib_activations(layer: Layer, x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    _dev(x, "x", torch.float32)
+    N = x.shape[0]
+    if out is None:
+        out = torch.empty((N, layer.m), dtype=torch.float32, device=x.device)
+    _dev(out, "out", torch.float32)
+    _check(raw().cats_calib_activations(layer.c, _ptr(x), N, _ptr(out), _stream()))
+    return out
+
+
+def threshold_from_acts(acts: torch.Tensor, sparsity: float, ws: Optional[torch.Tensor] = None) -> float:
+    _dev(acts, "acts", torch.float32)
+    if ws is None:
+        ws = torch.empty(4096, dtype=torch.uint8, device=acts.device)
+    t = _f32()
+    _check(raw().cats_threshold_from_acts(_ptr(acts), acts.numel(), float(sparsity), _ptr(ws),
+                                          ws.numel(), _stream(), ctypes.byref(t)))
+    return float(t.value)
+
+
+def calibrate_threshold(layer: Layer, calib_x: torch.Tensor, sparsity: float,
+                        ws: Optional[torch.Tensor] = None) -> float:
+    _dev(calib_x, "calib_x", torch.float32)
+    N = calib_x.shape[0]
+    if ws is None:
+        ws = workspace(layer.d, layer.m, 1, N * layer.m, device=calib_x.device)
+    t = _f32()
+    _check(raw().cats_calibrate_threshold(layer.c, _ptr(calib_x), N, float(sparsity), _ptr(ws),
+                                          ws.numel(), _stream(), ctypes.byref(t)))
+    return float(t.value)
+
+
+def _rows(x: torch.Tensor) -> int:
+    return 1 if x.dim() == 1 else int(x.shape[0])
+
+
+def mlp_forward(layer: Layer, x: torch.Tensor, t: float, residual: Optional[torch.Tensor] = None,
+                out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                aux: bool = False):
+    """CATS MLP forward.  Returns y, or (y, aux dict) when aux=True.
+
+    The aux dict holds per row b: idx[b, :cnt[b]] (ascending active neurons),
+    v and h (= v * x.W_up[:, j]) aligned with idx, and cnt.
+    """
+    _dev(x, "x", torch.float32)
+    B = _rows(x)
+    if out is None:
+        out = torch.empty_like(x)
+    _dev(out, "out", torch.float32)
+    if residual is not None:
+        _dev(residual, "residual", torch.float32)
+    if ws is None:
+        ws = workspace(layer.d, layer.m, B, device=x.device)
+    aux_c = None
+    bufs = None
+    if aux:
+        m = layer.m
+        bufs = {
+            "idx": torch.empty((B, m), dtype=torch.int32, device=x.device),
+            "cnt": torch.empty((B,), dtype=torch.int32, device=x.device),
+            "v": torch.empty((B, m), dtype=torch.float32, device=x.device),
+            "h": torch.empty((B, m), dtype=torch.float32, device=x.device),
+        }
+        aux_c = _Aux(bufs["idx"].data_ptr(), bufs["cnt"].data_ptr(), bufs["v"].data_ptr(),
+                     bufs["h"].data_ptr())
+    _check(raw().cats_mlp_forward(layer.c, _ptr(x), B, float(t), _ptr(residual), _ptr(out),
+                                  ctypes.byref(aux_c) if aux_c is not None else None, _ptr(ws),
+                                  ws.numel(), _stream()))
+    if aux:
+        return out, bufs
+    return out
+
+
+def mlp_dense(layer: Layer, x: torch.Tensor, residual: Optional[torch.Tensor] = None,
+              out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    _dev(x, "x", torch.float32)
+    B = _rows(x)
+    if out is None:
+        out = torch.empty_like(x)
+    _dev(out, "out", torch.float32)
+    if residual is not None:
+        _dev(residual, "residual", torch.float32)
+    if ws is None:
+        ws = workspace(layer.d, layer.m, B, device=x.device)
+    _check(raw().cats_mlp_dense(layer.c, _ptr(x), B, _ptr(residual), _ptr(out), _ptr(ws), ws.numel(),
+                                _stream()))
+    return out
+
+
+def rmsnorm(x: torch.Tensor, eps: float = 1e-5, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    _dev(x, "x", torch.float32)
+    if out is None:
+        out = torch.empty_like(x)
+    _dev(out, "out", torch.float32)
+    B = _rows(x)
+    d = int(x.shape[-1])
+    _check(raw().cats_rmsnorm(_ptr(x), _ptr(out), B, d, float(eps), _stream()))
+    return out
+
+
+def timer_enable(on: bool = True) -> None:
+    _check(raw().cats_timer_enable(1 if on else 0))
+
+
+def timer_reset() -> None:
+    _check(raw().cats_timer_reset())
+
+
+def timer_read() -> dict:
+    """{kernel name: (launches, total ms)} for the kernels timed so far."""
+    L = raw()
+    out = {}
+    for i in range(int(L.cats_timer_count())):
+        name = ctypes.c_char_p()
+        n = _i64()
+        ms = _f64()
+        _check(L.cats_timer_get(i, ctypes.byref(name), ctypes.byref(n), ctypes.byref(ms)))
+        out[name.value.decode()] = (int(n.value), float(ms.value))
+    return out

@@ -1,0 +1,492 @@
+// C ABI of libcats: argument validation (all on the host, before any HIP
+// call), workspace carving, kernel dispatch and the optional kernel timer.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "cats.h"
+#include "internal.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+cats_status fail(cats_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+cats_status hip_fail(hipError_t e, const char* what) {
+  return fail(CATS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+constexpr size_t kAlign = 256;
+constexpr size_t kRadixWords = 260;
+constexpr int kMaxBatchTile = 8;
+
+// Workspace regions.  The radix-select scratch always sits at offset 0;
+// the MLP region and the calibration activations share the space after it
+// (no call uses both).
+struct FwdLayout {
+  size_t partial, seg_j, seg_mask, seg_v, seg_h, seg_cnt, end;
+};
+
+size_t radix_bytes() { return round_up(kRadixWords * sizeof(uint32_t), kAlign); }
+
+FwdLayout fwd_layout(int d, int m, int bp) {
+  const int G = cats::fused_grid(m);
+  FwdLayout L;
+  size_t o = radix_bytes();
+  L.partial = o;
+  o = round_up(o + (size_t)G * bp * d * sizeof(float), kAlign);
+  L.seg_j = o;
+  o = round_up(o + (size_t)m * sizeof(int32_t), kAlign);
+  L.seg_mask = o;
+  o = round_up(o + (size_t)m * sizeof(uint32_t), kAlign);
+  L.seg_v = o;
+  o = round_up(o + (size_t)bp * m * sizeof(float), kAlign);
+  L.seg_h = o;
+  o = round_up(o + (size_t)bp * m * sizeof(float), kAlign);
+  L.seg_cnt = o;
+  o = round_up(o + (size_t)cats::kFusedBlocks * sizeof(int32_t), kAlign);
+  L.end = o;
+  return L;
+}
+
+size_t calib_bytes(int64_t nvalues) {
+  return radix_bytes() + round_up((size_t)nvalues * sizeof(float), kAlign);
+}
+
+bool d_ok(int32_t d, int32_t wdtype) {
+  if (d <= 0 || d % 8 != 0) return false;
+  return d <= (wdtype == CATS_BF16 ? CATS_MAX_D_BF16 : CATS_MAX_D_F32);
+}
+
+cats_status check_layer(const cats_layer* L) {
+  if (!L) return fail(CATS_ERR_NULL, "layer is NULL");
+  if (L->wdtype != CATS_F32 && L->wdtype != CATS_BF16)
+    return fail(CATS_ERR_DTYPE, "unknown weight dtype %d", (int)L->wdtype);
+  if (!d_ok(L->d, L->wdtype))
+    return fail(CATS_ERR_SHAPE, "d=%d must be a positive multiple of 8 and at most %d", (int)L->d,
+                L->wdtype == CATS_BF16 ? CATS_MAX_D_BF16 : CATS_MAX_D_F32);
+  if (L->m <= 0 || L->m > CATS_MAX_M)
+    return fail(CATS_ERR_SHAPE, "m=%d must be in [1, %d]", (int)L->m, CATS_MAX_M);
+  if (!L->w_gate_t || !L->w_up_t || !L->w_down) return fail(CATS_ERR_NULL, "a weight pointer is NULL");
+  if (!aligned(L->w_gate_t, 16) || !aligned(L->w_up_t, 16) || !aligned(L->w_down, 16))
+    return fail(CATS_ERR_ALIGN, "weight pointers must be 16-byte aligned");
+  const uint64_t mat = (uint64_t)L->m * L->d * (L->wdtype == CATS_BF16 ? 2 : 4);
+  if (mat > CATS_MAX_MATRIX_BYTES)
+    return fail(CATS_ERR_SHAPE, "each weight matrix must be at most %llu bytes (m*d*%d = %llu)",
+                (unsigned long long)CATS_MAX_MATRIX_BYTES, L->wdtype == CATS_BF16 ? 2 : 4,
+                (unsigned long long)mat);
+  return CATS_OK;
+}
+
+cats_status check_ws(const void* ws, size_t ws_bytes, size_t need) {
+  if (!ws) return fail(CATS_ERR_WORKSPACE, "workspace is NULL");
+  if (!aligned(ws, kAlign)) return fail(CATS_ERR_ALIGN, "workspace must be 256-byte aligned");
+  if (ws_bytes < need)
+    return fail(CATS_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  return CATS_OK;
+}
+
+int batch_tile(int rows) {
+  int bt = 1;
+  while (bt < rows) bt *= 2;
+  return bt;
+}
+
+// Shared body of forward and dense.
+cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, bool dense,
+                    const float* residual, float* y, const cats_forward_aux* aux, void* ws,
+                    size_t ws_bytes, void* stream) {
+  cats_status st = check_layer(L);
+  if (st != CATS_OK) return st;
+  if (!x || !y) return fail(CATS_ERR_NULL, "x or y is NULL");
+  if (B < 1 || B > CATS_MAX_BATCH) return fail(CATS_ERR_SHAPE, "B=%d outside [1, %d]", (int)B, CATS_MAX_BATCH);
+  if (!aligned(x, 16) || !aligned(y, 16) || (residual && !aligned(residual, 16)))
+    return fail(CATS_ERR_ALIGN, "x, y and residual must be 16-byte aligned");
+  if (std::isnan(t) || t < 0.f) return fail(CATS_ERR_RANGE, "t must be >= 0 (got %g)", (double)t);
+  const bool want_aux = aux && (aux->active_idx || aux->active_cnt || aux->active_v || aux->active_h);
+  if (want_aux && ((aux->active_idx && !aligned(aux->active_idx, 4)) ||
+                   (aux->active_cnt && !aligned(aux->active_cnt, 4)) ||
+                   (aux->active_v && !aligned(aux->active_v, 4)) ||
+                   (aux->active_h && !aligned(aux->active_h, 4))))
+    return fail(CATS_ERR_ALIGN, "aux outputs must be 4-byte aligned");
+  const int bf16 = L->wdtype == CATS_BF16;
+  const int d = L->d, m = L->m;
+  const int nch = cats::fused_nch(bf16, d);
+  const int bt_max = cats::fused_bt_max(bf16, nch);
+  const int rows_per_pass = B < bt_max ? B : bt_max;
+  const FwdLayout lay = fwd_layout(d, m, rows_per_pass);
+  st = check_ws(ws, ws_bytes, lay.end);
+  if (st != CATS_OK) return st;
+
+  char* w = static_cast<char*>(ws);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int G = cats::fused_grid(m);
+  for (int b0 = 0; b0 < B; b0 += rows_per_pass) {
+    const int bp = (B - b0) < rows_per_pass ? (B - b0) : rows_per_pass;
+    cats::FusedArgs fa;
+    fa.wg = L->w_gate_t;
+    fa.wu = L->w_up_t;
+    fa.wd = L->w_down;
+    fa.x = x + (size_t)b0 * d;
+    fa.B = bp;
+    fa.d = d;
+    fa.m = m;
+    fa.t = dense ? 0.f : t;
+    fa.partial = reinterpret_cast<float*>(w + lay.partial);
+    fa.aux = want_aux ? 1 : 0;
+    fa.seg_j = reinterpret_cast<int*>(w + lay.seg_j);
+    fa.seg_mask = reinterpret_cast<uint32_t*>(w + lay.seg_mask);
+    fa.seg_v = reinterpret_cast<float*>(w + lay.seg_v);
+    fa.seg_h = reinterpret_cast<float*>(w + lay.seg_h);
+    fa.seg_cnt = reinterpret_cast<int*>(w + lay.seg_cnt);
+    const int bt = batch_tile(bp);
+    hipError_t e;
+    if (bf16)
+      e = dense ? cats::launch_fused_bf16_dense(nch, bt, fa, G, s)
+          : fa.aux ? cats::launch_fused_bf16_cats_aux(nch, bt, fa, G, s)
+                   : cats::launch_fused_bf16_cats(nch, bt, fa, G, s);
+    else
+      e = dense ? cats::launch_fused_f32_dense(nch, bt, fa, G, s)
+          : fa.aux ? cats::launch_fused_f32_cats_aux(nch, bt, fa, G, s)
+                   : cats::launch_fused_f32_cats(nch, bt, fa, G, s);
+    if (e != hipSuccess) return hip_fail(e, "fused MLP launch");
+
+    cats::ReduceArgs ra;
+    ra.partial = fa.partial;
+    ra.G = G;
+    ra.B = bp;
+    ra.d = d;
+    ra.m = m;
+    ra.residual = residual ? residual + (size_t)b0 * d : nullptr;
+    ra.y = y + (size_t)b0 * d;
+    ra.aux = fa.aux;
+    ra.seg_j = fa.seg_j;
+    ra.seg_mask = fa.seg_mask;
+    ra.seg_v = fa.seg_v;
+    ra.seg_h = fa.seg_h;
+    ra.seg_cnt = fa.seg_cnt;
+    ra.active_idx = (want_aux && aux->active_idx) ? aux->active_idx + (size_t)b0 * m : nullptr;
+    ra.active_cnt = (want_aux && aux->active_cnt) ? aux->active_cnt + b0 : nullptr;
+    ra.active_v = (want_aux && aux->active_v) ? aux->active_v + (size_t)b0 * m : nullptr;
+    ra.active_h = (want_aux && aux->active_h) ? aux->active_h + (size_t)b0 * m : nullptr;
+    e = cats::launch_reduce(ra, s);
+    if (e != hipSuccess) return hip_fail(e, "reduce launch");
+  }
+  return CATS_OK;
+}
+
+int64_t cutoff_rank(int64_t n, double k) {
+  if (k == 0.0) return 0;
+  double r = std::ceil(k * (double)n - 1e-6);
+  if (r < 1) r = 1;
+  if (r > (double)n) r = (double)n;
+  return (int64_t)r;
+}
+
+cats_status select_threshold(const float* acts, int64_t n, double k, void* ws, hipStream_t s,
+                             float* t_out) {
+  const int64_t r = cutoff_rank(n, k);
+  if (r == 0) {
+    *t_out = 0.f;
+    return CATS_OK;
+  }
+  uint32_t* sc = static_cast<uint32_t*>(ws);
+  hipError_t e = cats::launch_radix_select(acts, n, r, sc, s);
+  if (e != hipSuccess) return hip_fail(e, "radix select launch");
+  uint32_t bits = 0;
+  e = hipMemcpyAsync(&bits, sc + 256, sizeof(bits), hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return hip_fail(e, "threshold copy");
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+  float t;
+  memcpy(&t, &bits, sizeof(t));
+  *t_out = t;
+  return CATS_OK;
+}
+
+// ---- kernel timer ---------------------------------------------------------
+struct TimerState {
+  std::mutex mu;
+  bool on = false;
+  std::vector<std::string> names;
+  std::vector<int64_t> launches;
+  std::vector<double> total_ms;
+  struct Pending {
+    int name;
+    hipEvent_t a, b;
+  };
+  std::vector<Pending> pending;
+  std::vector<hipEvent_t> pool;
+};
+
+TimerState& timer_state() {
+  static TimerState* st = new TimerState();  // lives until process exit
+  return *st;
+}
+
+int timer_name_index(TimerState& T, const char* name) {
+  for (size_t i = 0; i < T.names.size(); ++i)
+    if (T.names[i] == name) return (int)i;
+  T.names.emplace_back(name);
+  T.launches.push_back(0);
+  T.total_ms.push_back(0.0);
+  return (int)T.names.size() - 1;
+}
+
+hipError_t timer_flush_locked(TimerState& T) {
+  hipError_t first = hipSuccess;
+  for (auto& p : T.pending) {
+    hipError_t e = hipEventSynchronize(p.b);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.a, p.b);
+    if (e == hipSuccess) {
+      T.launches[p.name] += 1;
+      T.total_ms[p.name] += ms;
+    } else if (first == hipSuccess) {
+      first = e;
+    }
+    T.pool.push_back(p.a);
+    T.pool.push_back(p.b);
+  }
+  T.pending.clear();
+  return first;
+}
+
+hipEvent_t timer_event_locked(TimerState& T) {
+  if (!T.pool.empty()) {
+    hipEvent_t e = T.pool.back();
+    T.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+}  // namespace
+
+static_assert(CATS_MAX_M == cats::kMaxNeurons, "CATS_MAX_M must match the kernel's neuron capacity");
+
+namespace cats {
+
+int fused_nch(int wdtype_bf16, int d) {
+  const int need = (d + chunk_elems(wdtype_bf16) - 1) / chunk_elems(wdtype_bf16);
+  static const int inst[] = {1, 2, 4, 8, 10, 16};
+  for (int n : inst)
+    if (n >= need) return n;
+  return 16;
+}
+
+int fused_bt_max(int wdtype_bf16, int nch) {
+  const int row_bytes = nch * chunk_elems(wdtype_bf16) * (int)sizeof(float);
+  int bt = kMaxBatchTile;
+  while (bt > 1 && bt * row_bytes > kXLdsBytes) bt /= 2;
+  return bt;
+}
+
+int fused_grid(int m) { return m < kFusedBlocks ? m : kFusedBlocks; }
+
+KernelTimer::KernelTimer(const char* name, hipStream_t s) : slot_(-1), s_(s) {
+  TimerState& T = timer_state();
+  std::lock_guard<std::mutex> lk(T.mu);
+  if (!T.on) return;
+  if (T.pending.size() >= 4096) timer_flush_locked(T);
+  TimerState::Pending p;
+  p.name = timer_name_index(T, name);
+  p.a = timer_event_locked(T);
+  p.b = timer_event_locked(T);
+  if (!p.a || !p.b) return;
+  if (hipEventRecord(p.a, s) != hipSuccess) return;
+  T.pending.push_back(p);
+  slot_ = (int)T.pending.size() - 1;
+}
+
+KernelTimer::~KernelTimer() {
+  if (slot_ < 0) return;
+  TimerState& T = timer_state();
+  std::lock_guard<std::mutex> lk(T.mu);
+  if (slot_ < (int)T.pending.size()) (void)hipEventRecord(T.pending[slot_].b, s_);
+}
+
+}  // namespace cats
+
+extern "C" {
+
+int32_t cats_version(void) { return CATS_VERSION; }
+
+const char* cats_status_string(cats_status s) {
+  switch (s) {
+    case CATS_OK: return "ok";
+    case CATS_ERR_NULL: return "null pointer";
+    case CATS_ERR_SHAPE: return "unsupported shape";
+    case CATS_ERR_RANGE: return "argument out of range";
+    case CATS_ERR_DTYPE: return "unknown dtype";
+    case CATS_ERR_ALIGN: return "misaligned pointer";
+    case CATS_ERR_WORKSPACE: return "workspace missing or too small";
+    case CATS_ERR_HIP: return "HIP runtime error";
+    case CATS_ERR_UNIMPLEMENTED: return "not implemented";
+  }
+  return "unknown status";
+}
+
+const char* cats_last_error(void) { return g_last_error.c_str(); }
+
+size_t cats_workspace_bytes(int32_t d, int32_t m, int32_t max_batch, int64_t max_calib_values) {
+  if (d <= 0 || d % 8 != 0 || d > CATS_MAX_D_BF16 || m <= 0 || m > CATS_MAX_M || max_batch < 1 ||
+      max_batch > CATS_MAX_BATCH || max_calib_values < 0)
+    return 0;
+  const int bp = max_batch < kMaxBatchTile ? max_batch : kMaxBatchTile;
+  const size_t fwd = fwd_layout(d, m, bp).end;
+  const size_t cal = calib_bytes(max_calib_values);
+  return fwd > cal ? fwd : cal;
+}
+
+cats_status cats_pack_weights(const void* w, void* w_t, int32_t rows, int32_t cols, int32_t dtype,
+                              void* stream) {
+  if (!w || !w_t) return fail(CATS_ERR_NULL, "w or w_t is NULL");
+  if (dtype != CATS_F32 && dtype != CATS_BF16) return fail(CATS_ERR_DTYPE, "unknown dtype %d", (int)dtype);
+  if (rows <= 0 || cols <= 0 || rows > (65535 * 32)) return fail(CATS_ERR_SHAPE, "bad shape %d x %d", (int)rows, (int)cols);
+  const int eb = dtype == CATS_BF16 ? 2 : 4;
+  if (!aligned(w, eb) || !aligned(w_t, eb)) return fail(CATS_ERR_ALIGN, "w and w_t must be element-aligned");
+  const size_t bytes = (size_t)rows * cols * eb;
+  const char* a = static_cast<const char*>(w);
+  const char* b = static_cast<const char*>(w_t);
+  if (a < b + bytes && b < a + bytes) return fail(CATS_ERR_RANGE, "w and w_t overlap");
+  hipError_t e = cats::launch_transpose(w, w_t, rows, cols, eb, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "transpose launch");
+  return CATS_OK;
+}
+
+cats_status cats_calib_activations(const cats_layer* layer, const float* x, int32_t N, float* acts,
+                                   void* stream) {
+  cats_status st = check_layer(layer);
+  if (st != CATS_OK) return st;
+  if (!x || !acts) return fail(CATS_ERR_NULL, "x or acts is NULL");
+  if (N <= 0 || N > 4 * 1024 * 1024) return fail(CATS_ERR_SHAPE, "N=%d out of range", (int)N);
+  if (!aligned(x, 16) || !aligned(acts, 4)) return fail(CATS_ERR_ALIGN, "x must be 16-byte and acts 4-byte aligned");
+  hipError_t e = cats::launch_calib_acts(layer->wdtype == CATS_BF16, x, layer->w_gate_t, N, layer->d,
+                                         layer->m, acts, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "calibration activations launch");
+  return CATS_OK;
+}
+
+cats_status cats_threshold_from_acts(const float* acts, int64_t n, double sparsity, void* ws,
+                                     size_t ws_bytes, void* stream, float* t_out) {
+  if (!acts || !t_out) return fail(CATS_ERR_NULL, "acts or t_out is NULL");
+  if (n <= 0 || n > (int64_t)0xffffffffll) return fail(CATS_ERR_SHAPE, "n=%lld out of range", (long long)n);
+  if (!std::isfinite(sparsity) || sparsity < 0.0 || sparsity > 1.0)
+    return fail(CATS_ERR_RANGE, "sparsity must be in [0, 1]");
+  if (!aligned(acts, 4)) return fail(CATS_ERR_ALIGN, "acts must be 4-byte aligned");
+  if (sparsity == 0.0) {
+    *t_out = 0.f;
+    return CATS_OK;
+  }
+  cats_status st = check_ws(ws, ws_bytes, radix_bytes());
+  if (st != CATS_OK) return st;
+  return select_threshold(acts, n, sparsity, ws, static_cast<hipStream_t>(stream), t_out);
+}
+
+cats_status cats_calibrate_threshold(const cats_layer* layer, const float* calib_x, int32_t N,
+                                     double sparsity, void* ws, size_t ws_bytes, void* stream,
+                                     float* t_out) {
+  cats_status st = check_layer(layer);
+  if (st != CATS_OK) return st;
+  if (!calib_x || !t_out) return fail(CATS_ERR_NULL, "calib_x or t_out is NULL");
+  if (N <= 0 || N > 4 * 1024 * 1024) return fail(CATS_ERR_SHAPE, "N=%d out of range", (int)N);
+  if (!aligned(calib_x, 16)) return fail(CATS_ERR_ALIGN, "calib_x must be 16-byte aligned");
+  if (!std::isfinite(sparsity) || sparsity < 0.0 || sparsity > 1.0)
+    return fail(CATS_ERR_RANGE, "sparsity must be in [0, 1]");
+  const int64_t n = (int64_t)N * layer->m;
+  if (n > (int64_t)0xffffffffll) return fail(CATS_ERR_SHAPE, "N*m=%lld too large", (long long)n);
+  if (sparsity == 0.0) {
+    *t_out = 0.f;
+    return CATS_OK;
+  }
+  st = check_ws(ws, ws_bytes, calib_bytes(n));
+  if (st != CATS_OK) return st;
+  float* acts = reinterpret_cast<float*>(static_cast<char*>(ws) + radix_bytes());
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = cats::launch_calib_acts(layer->wdtype == CATS_BF16, calib_x, layer->w_gate_t, N,
+                                         layer->d, layer->m, acts, s);
+  if (e != hipSuccess) return hip_fail(e, "calibration activations launch");
+  return select_threshold(acts, n, sparsity, ws, s, t_out);
+}
+
+cats_status cats_mlp_forward(const cats_layer* layer, const float* x, int32_t B, float t,
+                             const float* residual, float* y, const cats_forward_aux* aux, void* ws,
+                             size_t ws_bytes, void* stream) {
+  return run_mlp(layer, x, B, t, false, residual, y, aux, ws, ws_bytes, stream);
+}
+
+cats_status cats_mlp_dense(const cats_layer* layer, const float* x, int32_t B, const float* residual,
+                           float* y, void* ws, size_t ws_bytes, void* stream) {
+  return run_mlp(layer, x, B, 0.f, true, residual, y, nullptr, ws, ws_bytes, stream);
+}
+
+cats_status cats_rmsnorm(const float* x, float* xn, int32_t B, int32_t d, float eps, void* stream) {
+  if (!x || !xn) return fail(CATS_ERR_NULL, "x or xn is NULL");
+  if (B < 1 || B > 65535 || d < 1) return fail(CATS_ERR_SHAPE, "B=%d, d=%d out of range", (int)B, (int)d);
+  if (std::isnan(eps) || eps < 0.f) return fail(CATS_ERR_RANGE, "eps must be >= 0");
+  if (!aligned(x, 4) || !aligned(xn, 4)) return fail(CATS_ERR_ALIGN, "x and xn must be 4-byte aligned");
+  hipError_t e = cats::launch_rmsnorm(x, xn, B, d, eps, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "rmsnorm launch");
+  return CATS_OK;
+}
+
+cats_status cats_timer_enable(int32_t on) {
+  TimerState& T = timer_state();
+  std::lock_guard<std::mutex> lk(T.mu);
+  T.on = on != 0;
+  return CATS_OK;
+}
+
+cats_status cats_timer_reset(void) {
+  TimerState& T = timer_state();
+  std::lock_guard<std::mutex> lk(T.mu);
+  hipError_t e = T.pending.empty() ? hipSuccess : timer_flush_locked(T);
+  for (size_t i = 0; i < T.names.size(); ++i) {
+    T.launches[i] = 0;
+    T.total_ms[i] = 0.0;
+  }
+  if (e != hipSuccess) return hip_fail(e, "timer flush");
+  return CATS_OK;
+}
+
+int32_t cats_timer_count(void) {
+  TimerState& T = timer_state();
+  std::lock_guard<std::mutex> lk(T.mu);
+  return (int32_t)T.names.size();
+}
+
+cats_status cats_timer_get(int32_t i, const char** name, int64_t* launches, double* total_ms) {
+  TimerState& T = timer_state();
+  std::lock_guard<std::mutex> lk(T.mu);
+  if (i < 0 || i >= (int32_t)T.names.size()) return fail(CATS_ERR_RANGE, "timer index %d out of range", (int)i);
+  hipError_t e = T.pending.empty() ? hipSuccess : timer_flush_locked(T);
+  if (e != hipSuccess) return hip_fail(e, "timer flush");
+  if (name) *name = T.names[i].c_str();
+  if (launches) *launches = T.launches[i];
+  if (total_ms) *total_ms = T.total_ms[i];
+  return CATS_OK;
+}
+
+}  // extern "C"

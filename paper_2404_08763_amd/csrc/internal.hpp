@@ -1,0 +1,100 @@
+// Host-side interface between the C ABI (cats_api.cpp) and the kernel
+// translation units.  Every launcher assumes its arguments were validated.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace cats {
+
+// Waves per block of the fused MLP kernel.
+constexpr int kFusedWaves = 8;
+// Upper bound on fused-kernel blocks: one per compute unit of an MI355X.
+constexpr int kFusedBlocks = 256;
+// Neurons a fused-kernel block may own (its LDS lists are this long); with
+// kFusedBlocks blocks this bounds m.
+constexpr int kFusedMaxNeurons = 256;
+constexpr int kMaxNeurons = kFusedBlocks * kFusedMaxNeurons;
+// LDS bytes the fused kernel may spend on the staged x rows.
+constexpr int kXLdsBytes = 128 * 1024;
+
+// Elements per 64-lane chunk of a weight row (16 bytes per lane).
+inline int chunk_elems(int wdtype_bf16) { return wdtype_bf16 ? 512 : 256; }
+
+struct FusedArgs {
+  const void* wg;      // [m x d] W_gate^T
+  const void* wu;      // [m x d] W_up^T
+  const void* wd;      // [m x d] W_down
+  const float* x;      // [B x d]
+  int B, d, m;
+  float t;
+  float* partial;      // [G x B x d]
+  int aux;             // write the union segments for the aux outputs
+  int* seg_j;          // [m]
+  uint32_t* seg_mask;  // [m] bit b = active in row b
+  float* seg_v;        // [B x m]
+  float* seg_h;        // [B x m]
+  int* seg_cnt;        // [G]
+};
+
+struct ReduceArgs {
+  const float* partial;  // [G x B x d]
+  int G, B, d, m;
+  const float* residual;  // [B x d] or null
+  float* y;               // [B x d]
+  // aux (finalize) part; all null when not requested
+  int aux;
+  const int* seg_j;
+  const uint32_t* seg_mask;
+  const float* seg_v;
+  const float* seg_h;
+  const int* seg_cnt;
+  int* active_idx;
+  int* active_cnt;
+  float* active_v;
+  float* active_h;
+};
+
+// Instantiated chunk counts per row (NCH); a row of d elements uses the
+// smallest instantiated NCH >= ceil(d / chunk).
+int fused_nch(int wdtype_bf16, int d);
+// Largest batch tile (1, 2, 4 or 8) whose x rows fit the LDS budget.
+int fused_bt_max(int wdtype_bf16, int nch);
+// Blocks of the fused kernel: block g owns neurons [g*m/G, (g+1)*m/G).
+int fused_grid(int m);
+
+// Fused-kernel launchers per weight type and variant (cats, cats with the
+// active-list segments, dense).
+hipError_t launch_fused_bf16_cats(int nch, int bt, const FusedArgs& a, int G, hipStream_t s);
+hipError_t launch_fused_bf16_cats_aux(int nch, int bt, const FusedArgs& a, int G, hipStream_t s);
+hipError_t launch_fused_bf16_dense(int nch, int bt, const FusedArgs& a, int G, hipStream_t s);
+hipError_t launch_fused_f32_cats(int nch, int bt, const FusedArgs& a, int G, hipStream_t s);
+hipError_t launch_fused_f32_cats_aux(int nch, int bt, const FusedArgs& a, int G, hipStream_t s);
+hipError_t launch_fused_f32_dense(int nch, int bt, const FusedArgs& a, int G, hipStream_t s);
+hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
+
+hipError_t launch_calib_acts(int wdtype_bf16, const float* x, const void* wg_t, int N, int d,
+                             int m, float* acts, hipStream_t s);
+// Radix select of the r-th smallest |a| (1-indexed) over n fp32 values;
+// `scratch` holds 260 words.  The selected bit pattern ends in scratch[256].
+hipError_t launch_radix_select(const float* a, int64_t n, int64_t r, uint32_t* scratch,
+                               hipStream_t s);
+
+hipError_t launch_rmsnorm(const float* x, float* xn, int B, int d, float eps, hipStream_t s);
+hipError_t launch_transpose(const void* in, void* out, int rows, int cols, int elem_bytes,
+                            hipStream_t s);
+
+// Optional per-kernel timing (cats_timer_*): a scope that records HIP events
+// around one launch on its stream while the timer is enabled.
+class KernelTimer {
+ public:
+  KernelTimer(const char* name, hipStream_t s);
+  ~KernelTimer();
+
+ private:
+  int slot_;
+  hipStream_t s_;
+};
+
+}  // namespace cats

@@ -1,0 +1,10 @@
+// Instantiations of the fused MLP kernel: bf16 weights, cats variant.
+#include "mlp_fused.hpp"
+
+namespace cats {
+
+hipError_t launch_fused_bf16_cats(int nch, int bt, const FusedArgs& a, int G, hipStream_t s) {
+  return launch_fused_t<wbf16, false, false>(nch, bt, a, G, s);
+}
+
+}  // namespace cats

@@ -1,0 +1,174 @@
+"""The C ABI contract on the CPU: the library loads, exports every declared
+symbol, and rejects bad arguments on the host before any HIP call.
+
+Fake device addresses are passed where validation must fail first; they are
+never dereferenced.
+"""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2404_08763_amd as P
+from paper_2404_08763_amd import _lib
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "cats.h")
+
+OK, NULL, SHAPE, RANGE, DTYPE, ALIGN, WORKSPACE, HIP = 0, 1, 2, 3, 4, 5, 6, 7
+A = 0x100000  # fake, aligned device addresses (never dereferenced)
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cats_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    L = P.raw()
+    names = _declared()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_strings():
+    L = P.raw()
+    assert L.cats_version() == 1
+    for s in range(9):
+        assert L.cats_status_string(s)
+    assert L.cats_status_string(99) == b"unknown status"
+
+
+def _layer(d=64, m=96, dtype=P.CATS_BF16, wg=A, wu=A + 4096, wd=A + 8192):
+    return _lib._Layer(d, m, dtype, wg, wu, wd)
+
+
+def _fwd(layer, x=A, B=1, t=0.5, res=None, y=A + 65536, ws=A * 4, ws_bytes=1 << 30):
+    L = P.raw()
+    return L.cats_mlp_forward(ctypes.byref(layer) if layer is not None else None, ctypes.c_void_p(x), B,
+                              ctypes.c_float(t), ctypes.c_void_p(res) if res else None, ctypes.c_void_p(y),
+                              None, ctypes.c_void_p(ws) if ws else None, ws_bytes, None)
+
+
+def test_forward_validation():
+    assert _fwd(None) == NULL
+    assert _fwd(_layer(d=0)) == SHAPE
+    assert _fwd(_layer(d=12)) == SHAPE
+    assert _fwd(_layer(d=8192 + 8)) == SHAPE
+    assert _fwd(_layer(d=4096 + 8, dtype=P.CATS_F32)) == SHAPE
+    assert _fwd(_layer(m=0)) == SHAPE
+    assert _fwd(_layer(dtype=7)) == DTYPE
+    assert _fwd(_layer(wg=0)) == NULL
+    assert _fwd(_layer(wd=A + 2)) == ALIGN
+    assert _fwd(_layer(), x=0) == NULL
+    assert _fwd(_layer(), y=0) == NULL
+    assert _fwd(_layer(), x=A + 4) == ALIGN
+    assert _fwd(_layer(), res=A + 8) == ALIGN
+    assert _fwd(_layer(), B=0) == SHAPE
+    assert _fwd(_layer(), B=17) == SHAPE
+    assert _fwd(_layer(), t=-1.0) == RANGE
+    assert _fwd(_layer(), t=float("nan")) == RANGE
+    assert _fwd(_layer(), ws=0) == WORKSPACE
+    assert _fwd(_layer(), ws=A + 64) == ALIGN
+    need = P.workspace_bytes(64, 96, 1, 0)
+    assert _fwd(_layer(), ws_bytes=need - 1) == WORKSPACE
+    assert b"workspace" in P.raw().cats_last_error()
+
+
+def test_dense_validation():
+    L = P.raw()
+    lay = _layer()
+    st = L.cats_mlp_dense(ctypes.byref(lay), None, 1, None, ctypes.c_void_p(A), ctypes.c_void_p(A * 4), 1 << 30, None)
+    assert st == NULL
+    st = L.cats_mlp_dense(ctypes.byref(lay), ctypes.c_void_p(A), 1, None, ctypes.c_void_p(A), ctypes.c_void_p(A * 4), 16, None)
+    assert st == WORKSPACE
+
+
+def test_workspace_bytes():
+    assert P.workspace_bytes(0, 10, 1, 0) == 0
+    assert P.workspace_bytes(12, 10, 1, 0) == 0
+    assert P.workspace_bytes(64, 0, 1, 0) == 0
+    assert P.workspace_bytes(64, 10, 0, 0) == 0
+    assert P.workspace_bytes(64, 10, 17, 0) == 0
+    assert P.workspace_bytes(64, 10, 1, -1) == 0
+    a = P.workspace_bytes(4096, 11008, 1, 0)
+    b = P.workspace_bytes(4096, 11008, 8, 0)
+    c = P.workspace_bytes(4096, 11008, 16, 0)
+    assert 0 < a < b <= c
+    assert P.workspace_bytes(4096, 11008, 1, 2048 * 11008) >= 2048 * 11008 * 4
+    assert a % 256 == 0
+
+
+def test_threshold_validation():
+    L = P.raw()
+    t = ctypes.c_float(-1.0)
+
+    def call(acts=A, n=100, k=0.5, ws=A * 4, ws_bytes=4096):
+        return L.cats_threshold_from_acts(ctypes.c_void_p(acts) if acts else None, n, k,
+                                          ctypes.c_void_p(ws) if ws else None, ws_bytes, None, ctypes.byref(t))
+
+    assert call(acts=0) == NULL
+    assert call(n=0) == SHAPE
+    assert call(n=1 << 33) == SHAPE
+    assert call(k=1.5) == RANGE
+    assert call(k=-0.1) == RANGE
+    assert call(k=float("nan")) == RANGE
+    assert call(acts=A + 2) == ALIGN
+    assert call(ws=0) == WORKSPACE
+    assert call(ws_bytes=16) == WORKSPACE
+    # k = 0 is answered on the host: t = 0 without touching the (fake) buffers
+    assert call(k=0.0) == OK and t.value == 0.0
+
+
+def test_calibrate_validation():
+    L = P.raw()
+    t = ctypes.c_float()
+    lay = _layer(d=4096, m=11008)
+
+    def call(x=A, N=16, k=0.5, ws_bytes=1 << 40, layer=lay):
+        return L.cats_calibrate_threshold(ctypes.byref(layer), ctypes.c_void_p(x) if x else None, N, k,
+                                          ctypes.c_void_p(A * 4), ws_bytes, None, ctypes.byref(t))
+
+    assert call(x=0) == NULL
+    assert call(N=0) == SHAPE
+    assert call(N=400000) == SHAPE  # N * m above 2^32
+    assert call(k=2.0) == RANGE
+    assert call(x=A + 4) == ALIGN
+    assert call(ws_bytes=1024) == WORKSPACE
+    assert call(k=0.0) == OK and t.value == 0.0
+    st = L.cats_calib_activations(ctypes.byref(lay), None, 16, ctypes.c_void_p(A), None)
+    assert st == NULL
+
+
+def test_pack_and_rmsnorm_validation():
+    L = P.raw()
+    assert L.cats_pack_weights(None, ctypes.c_void_p(A), 4, 4, 1, None) == NULL
+    assert L.cats_pack_weights(ctypes.c_void_p(A), ctypes.c_void_p(A * 2), 4, 4, 3, None) == DTYPE
+    assert L.cats_pack_weights(ctypes.c_void_p(A), ctypes.c_void_p(A * 2), 0, 4, 1, None) == SHAPE
+    assert L.cats_pack_weights(ctypes.c_void_p(A), ctypes.c_void_p(A + 8), 64, 64, 1, None) == RANGE
+    assert L.cats_pack_weights(ctypes.c_void_p(A + 1), ctypes.c_void_p(A * 2), 4, 4, 1, None) == ALIGN
+    f = ctypes.c_float
+    assert L.cats_rmsnorm(None, ctypes.c_void_p(A), 1, 8, f(1e-5), None) == NULL
+    assert L.cats_rmsnorm(ctypes.c_void_p(A), ctypes.c_void_p(A), 0, 8, f(1e-5), None) == SHAPE
+    assert L.cats_rmsnorm(ctypes.c_void_p(A), ctypes.c_void_p(A), 1, 8, f(-1.0), None) == RANGE
+    assert L.cats_rmsnorm(ctypes.c_void_p(A), ctypes.c_void_p(A), 1, 8, f(math.nan), None) == RANGE
+
+
+def test_timer_interface_without_device():
+    L = P.raw()
+    assert L.cats_timer_enable(0) == OK
+    assert L.cats_timer_reset() == OK
+    n = L.cats_timer_count()
+    name = ctypes.c_char_p()
+    assert L.cats_timer_get(n + 5, ctypes.byref(name), None, None) == RANGE
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"), reason="only meaningful without a GPU")
+def test_no_device_is_a_hip_error_not_a_crash():
+    L = P.raw()
+    st = L.cats_rmsnorm(ctypes.c_void_p(A), ctypes.c_void_p(A * 2), 1, 64, ctypes.c_float(1e-5), None)
+    assert st == HIP
+    assert L.cats_last_error()

@@ -1,0 +1,284 @@
+"""Device path (libcats through the C ABI) against the CPU oracle.
+
+Same seeded inputs on both sides; the oracle is the fp32 build.  Bars:
+  - active sets identical except neurons with ||v| - t| <= 1e-3 t
+  - y within 2e-2 * ||y_oracle||_inf (measured errors are far smaller)
+  - index work (pack, threshold selection) bit-exact
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2404_08763_amd as P
+from paper_2404_08763_amd import workloads as W
+
+from gpu_util import check_forward, device_layer, host_f32, quantile_t, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a device"
+    return torch.device("cuda:0")
+
+
+def test_single_hip_runtime(dev):
+    """libcats binds to the HIP runtime torch loaded (one copy in the process)."""
+    P.raw()
+    torch.zeros(1, device=dev)
+    maps = open("/proc/self/maps").read().splitlines()
+    paths = {ln.split()[-1] for ln in maps if "libamdhip64" in ln}
+    assert len(paths) == 1, paths
+    assert any(P.lib_path() in ln for ln in maps)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("shape", [(37, 53), (4096, 688), (1, 9), (256, 688)])
+def test_pack_bit_exact(dev, dtype, shape):
+    say("pack", dtype, shape)
+    g = torch.Generator().manual_seed(5)
+    w = torch.randn(shape, generator=g).to(dtype)
+    out = P.pack_weights(w.to(dev)).cpu()
+    ref = w.t().contiguous()
+    assert torch.equal(out.view(torch.int16 if dtype == torch.bfloat16 else torch.int32),
+                       ref.view(torch.int16 if dtype == torch.bfloat16 else torch.int32))
+
+
+# ---------------------------------------------------------------- C1 (tiny)
+@pytest.fixture(scope="module")
+def c1(dev, oracle32):
+    c = W.CONFIGS["C1"]
+    wg, wu, wd = W.weights(c.d, c.m, c.wdtype)
+    layer = device_layer(wg, wu, wd)
+    hw = host_f32(wg, wu, wd)
+    xcal = W.calib_vectors(c)
+    acts = oracle32.calib_acts(xcal.numpy(), hw[0])
+    t = oracle32.threshold(acts, 0.5)
+    return c, layer, hw, xcal, acts, t
+
+
+def test_c1_forward_all_vectors(c1, oracle32):
+    c, layer, hw, _, _, t = c1
+    xs = W.decode_vectors(c)
+    ws = P.workspace(c.d, c.m, 1)
+    flips = 0
+    for i in range(c.n_decode):
+        say("C1 forward vector", i, "t", t)
+        x = xs[i : i + 1].contiguous()
+        y, aux = P.mlp_forward(layer, x.cuda(), t, ws=ws, aux=True)
+        ref = oracle32.cats_mlp(x.numpy(), *hw, t=t)
+        ref_all = oracle32.cats_mlp(x.numpy(), *hw, t=0.0)
+        flips += check_forward(y, aux, ref, t, 1, f"C1[{i}]", ref_all=ref_all, w_down=hw[2])["band_flips"]
+    assert flips <= 3
+
+
+def test_c1_dense_and_t0(c1, oracle32):
+    c, layer, hw, _, _, _ = c1
+    x = W.decode_vectors(c, 4)
+    say("C1 dense B=4")
+    yd = P.mlp_dense(layer, x.cuda())
+    ref = oracle32.cats_mlp(x.numpy(), *hw, t=0.0, dense=True)
+    check_forward(yd, None, ref, 0.0, 4, "C1 dense")
+    say("C1 forward t=0 B=4")
+    y0 = P.mlp_forward(layer, x.cuda(), 0.0)
+    assert torch.equal(y0.view(torch.int32), yd.view(torch.int32)), "t=0 must equal dense bit for bit"
+
+
+def test_c1_calibration(c1, oracle32):
+    c, layer, hw, xcal, acts_o, t_o = c1
+    say("C1 calibrate")
+    xg = xcal.cuda()
+    acts = P.calib_activations(layer, xg)
+    a = acts.cpu().double().numpy()
+    assert np.abs(a - acts_o).max() <= 1e-5 * acts_o.max()
+    t = P.calibrate_threshold(layer, xg, 0.5)
+    assert abs(t - t_o) <= 1e-3 * t_o, (t, t_o)
+    # the rank invariant of Eq. 3 on the device's own activations
+    s = np.sort(a.ravel())
+    n = s.size
+    r = int(np.ceil(0.5 * n - 1e-6))
+    assert t == np.float32(s[r - 1])
+    assert int(np.sum(s < t)) <= r - 1 < 0.5 * n <= r <= int(np.sum(s <= t))
+
+
+# ------------------------------------------- small bf16 shapes, ragged tails
+@pytest.mark.parametrize("d,m", [(1032, 693), (512, 1000), (8, 7), (4096, 97), (5120, 300), (8192, 64)])
+def test_bf16_ragged_shapes(dev, oracle32, d, m):
+    c = W.shrink(W.CONFIGS["C2"], d, m)
+    wg, wu, wd = W.weights(d, m, torch.bfloat16, layer=3)
+    layer = device_layer(wg, wu, wd)
+    hw = host_f32(wg, wu, wd)
+    x = W.decode_vectors(c, 3)
+    all0 = [oracle32.cats_mlp(x[b : b + 1].numpy(), *hw, t=0.0) for b in range(3)]
+    v0 = np.concatenate([r["v"] for r in all0], axis=0)
+    for k in (0.5, 0.9):
+        t = quantile_t(np.abs(v0), k)
+        say("ragged", d, m, "k", k, "t", t)
+        for b in range(3):
+            xb = x[b : b + 1].contiguous()
+            y, aux = P.mlp_forward(layer, xb.cuda(), t, aux=True)
+            ref = oracle32.cats_mlp(xb.numpy(), *hw, t=t)
+            check_forward(y, aux, ref, t, 1, f"d{d} m{m} k{k} b{b}", ref_all=all0[b], w_down=hw[2])
+
+
+@pytest.mark.parametrize("B", [2, 3, 4, 8, 16])
+def test_batch_rows_have_their_own_masks(dev, oracle32, B):
+    d, m = 1024, 1500
+    c = W.shrink(W.CONFIGS["C3"], d, m)
+    wg, wu, wd = W.weights(d, m, torch.bfloat16, layer=4)
+    layer = device_layer(wg, wu, wd)
+    hw = host_f32(wg, wu, wd)
+    x = W.decode_vectors(c, B)
+    ref_all = oracle32.cats_mlp(x.numpy(), *hw, t=0.0)
+    t = quantile_t(np.abs(ref_all["v"]), 0.7)
+    res = torch.randn((B, d), generator=torch.Generator().manual_seed(9))
+    say("batch", B, "t", t)
+    y, aux = P.mlp_forward(layer, x.cuda(), t, residual=res.cuda(), aux=True)
+    ref = oracle32.cats_mlp(x.numpy(), *hw, t=t, residual=res.numpy())
+    check_forward(y, aux, ref, t, B, f"B{B}", ref_all=ref_all, w_down=hw[2])
+    # rows differ in their masks (contextual sparsity)
+    cnt = aux["cnt"].cpu().numpy()
+    assert len(set(cnt.tolist())) > 1 or B == 1
+    # each row equals its own batch-1 call bit for bit
+    for b in range(B):
+        yb = P.mlp_forward(layer, x[b : b + 1].cuda(), t, residual=res[b : b + 1].cuda())
+        assert torch.equal(yb.view(torch.int32), y[b : b + 1].view(torch.int32))
+
+
+# ------------------------------------------------------ edge cases (C1 size)
+def test_edges(c1, oracle32):
+    c, layer, hw, _, _, _ = c1
+    x = W.decode_vectors(c, 1)
+    xg = x.cuda()
+    res = torch.randn((1, c.d), generator=torch.Generator().manual_seed(2)).cuda()
+    say("edges: t=inf")
+    y, aux = P.mlp_forward(layer, xg, float("inf"), aux=True)
+    assert int(aux["cnt"][0]) == 0
+    assert torch.all(y == 0) and not torch.any(torch.signbit(y))
+    y = P.mlp_forward(layer, xg, float("inf"), residual=res)
+    assert torch.equal(y, res)
+    say("edges: t=0 all active")
+    y, aux = P.mlp_forward(layer, xg, 0.0, aux=True)
+    assert int(aux["cnt"][0]) == c.m
+    assert torch.equal(aux["idx"][0].cpu(), torch.arange(c.m, dtype=torch.int32))
+    say("edges: one active neuron")
+    v = oracle32.cats_mlp(x.numpy(), *hw, t=0.0)["v"][0]
+    order = np.argsort(np.abs(v))
+    t = float(0.5 * (abs(v[order[-1]]) + abs(v[order[-2]])))
+    y, aux = P.mlp_forward(layer, xg, t, aux=True)
+    assert int(aux["cnt"][0]) == 1 and int(aux["idx"][0, 0]) == int(order[-1])
+    j = int(order[-1])
+    h = aux["h"][0, 0].cpu()
+    expect = h * torch.from_numpy(hw[2][j])  # fp32 product, rounded once
+    assert torch.equal(y[0].cpu(), expect)
+
+
+def test_determinism_and_aux_invariance(c1):
+    c, layer, hw, _, _, t = c1
+    x = W.decode_vectors(c, 8).cuda()
+    say("determinism")
+    y1, a1 = P.mlp_forward(layer, x, t, aux=True)
+    y2, a2 = P.mlp_forward(layer, x, t, aux=True)
+    y3 = P.mlp_forward(layer, x, t)
+    assert torch.equal(y1.view(torch.int32), y2.view(torch.int32))
+    assert torch.equal(y1.view(torch.int32), y3.view(torch.int32))
+    for k in ("cnt", "idx", "v", "h"):
+        if k == "cnt":
+            assert torch.equal(a1[k], a2[k])
+        else:
+            for b in range(8):
+                n = int(a1["cnt"][b])
+                assert torch.equal(a1[k][b, :n], a2[k][b, :n])
+
+
+def test_rmsnorm(dev, oracle32):
+    for B, d in ((1, 4096), (3, 5120), (2, 7)):
+        say("rmsnorm", B, d)
+        x = torch.randn((B, d), generator=torch.Generator().manual_seed(d)) * 3
+        y = P.rmsnorm(x.cuda(), 1e-5).cpu().double().numpy()
+        ref = oracle32.rmsnorm(x.numpy(), 1e-5)
+        assert np.abs(y - ref).max() <= 2e-6 * np.abs(ref).max()
+
+
+def test_threshold_from_acts_bit_exact(dev, oracle32):
+    g = torch.Generator().manual_seed(31)
+    for n in (1, 7, 1000, 1 << 20, 3_000_001):
+        a = torch.randn(n, generator=g)
+        if n > 10:
+            a[::13] = a[5]
+            a[1::17] = -a[9]
+        ag = a.cuda()
+        for k in (0.0, 1e-6, 0.3, 0.5, 0.7, 0.9, 1.0):
+            say("threshold n", n, "k", k)
+            t = P.threshold_from_acts(ag, k)
+            to = oracle32.threshold(a.double().numpy(), k)
+            assert np.float32(t) == np.float32(to), (n, k, t, to)
+
+
+# --------------------------------------- full-size shapes (sampled oracle)
+@pytest.fixture(scope="module")
+def big(dev):
+    cache = {}
+
+    def get(name):
+        if name not in cache:
+            cache.clear()
+            c = W.CONFIGS[name]
+            wg, wu, wd = W.weights(c.d, c.m, c.wdtype)
+            cache[name] = (c, device_layer(wg, wu, wd), host_f32(wg, wu, wd))
+        return cache[name]
+
+    return get
+
+
+@pytest.mark.parametrize("name,ks", [("C2", (0.5, 0.7, 0.9)), ("C3", (0.0, 0.3, 0.5, 0.7, 0.9))])
+def test_full_size_forward(big, oracle32, name, ks):
+    c, layer, hw = big(name)
+    x = W.decode_vectors(c, 2)
+    ws = P.workspace(c.d, c.m, 1)
+    refs0 = [oracle32.cats_mlp(x[i : i + 1].numpy(), *hw, t=0.0) for i in range(2)]
+    vall = np.concatenate([r["v"] for r in refs0], axis=0)
+    for k in ks:
+        t = quantile_t(np.abs(vall), k) if k > 0 else 0.0
+        for i in range(2):
+            say(name, "full-size forward k", k, "token", i, "t", t)
+            xi = x[i : i + 1].contiguous()
+            y, aux = P.mlp_forward(layer, xi.cuda(), t, ws=ws, aux=True)
+            ref = refs0[i] if k == 0 else oracle32.cats_mlp(xi.numpy(), *hw, t=t)
+            check_forward(y, aux, ref, t, 1, f"{name} k{k} tok{i}", ref_all=refs0[i], w_down=hw[2])
+            y_noaux = P.mlp_forward(layer, xi.cuda(), t, ws=ws)  # the benchmark's configuration
+            assert torch.equal(y.view(torch.int32), y_noaux.view(torch.int32))
+
+
+def test_full_size_dense(big, oracle32):
+    c, layer, hw = big("C2")
+    x = W.decode_vectors(c, 1)
+    say("C2 dense")
+    y = P.mlp_dense(layer, x.cuda())
+    ref = oracle32.cats_mlp(x.numpy(), *hw, t=0.0, dense=True)
+    check_forward(y, None, ref, 0.0, 1, "C2 dense")
+
+
+def test_full_size_calibration_sampled(big, oracle32):
+    c, layer, hw = big("C2")
+    N = 256
+    xcal = W.calib_vectors(c, N)
+    say("C2 calibration activations N", N)
+    acts = P.calib_activations(layer, xcal.cuda()).cpu().double().numpy()
+    rng = np.random.default_rng(3)
+    pairs = np.stack([rng.integers(0, N, 3000), rng.integers(0, c.m, 3000)], axis=1)
+    ref = oracle32.calib_acts_at(xcal.numpy(), hw[0], pairs)
+    got = acts[pairs[:, 0], pairs[:, 1]]
+    assert np.abs(got - ref).max() <= 1e-5 * max(1.0, ref.max())
+    for k in (0.5, 0.7, 0.9):
+        say("C2 calibrate k", k)
+        t = P.calibrate_threshold(layer, xcal.cuda(), k)
+        s = np.sort(acts.ravel())
+        n = s.size
+        r = int(np.ceil(k * n - 1e-6))
+        assert t == np.float32(s[r - 1])  # exact order statistic of the device's activations
+        to = oracle32.threshold(acts, k)
+        assert t == np.float32(to)
