@@ -47,23 +47,28 @@ def _compile(src: str, extra: list[str]) -> str:
     return obj
 
 
-def build(jobs: int | None = None, extra: list[str] | None = None, verbose: bool = False) -> str:
-    """Compile every source and link libcats.so; returns its path."""
+def build(jobs: int | None = None, extra: list[str] | None = None, verbose: bool = False,
+          out: str | None = None, build_dir: str | None = None) -> str:
+    """Compile every source and link libcats.so (or `out`); returns its path."""
+    global BUILD
+    if build_dir:
+        BUILD = build_dir
+    lib = out or LIB
     os.makedirs(BUILD, exist_ok=True)
     extra = list(extra or [])
     srcs = sources()
     jobs = jobs or min(8, os.cpu_count() or 1, len(srcs))
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(lambda s: _compile(s, extra), srcs))
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {lib}")
+    return lib
 
 
 if __name__ == "__main__":

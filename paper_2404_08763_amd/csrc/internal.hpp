@@ -8,13 +8,19 @@
 
 namespace cats {
 
-// Waves per block of the fused MLP kernel.
-constexpr int kFusedWaves = 8;
-// Upper bound on fused-kernel blocks: one per compute unit of an MI355X.
-constexpr int kFusedBlocks = 256;
+// Geometry of the fused MLP kernel (build-time tunables): waves per block
+// and the number of blocks, one or two per compute unit of an MI355X.
+#ifndef CATS_FUSED_WAVES
+#define CATS_FUSED_WAVES 8
+#endif
+#ifndef CATS_FUSED_BLOCKS
+#define CATS_FUSED_BLOCKS 256
+#endif
+constexpr int kFusedWaves = CATS_FUSED_WAVES;
+constexpr int kFusedBlocks = CATS_FUSED_BLOCKS;
 // Neurons a fused-kernel block may own (its LDS lists are this long); with
 // kFusedBlocks blocks this bounds m.
-constexpr int kFusedMaxNeurons = 256;
+constexpr int kFusedMaxNeurons = 65536 / kFusedBlocks;
 constexpr int kMaxNeurons = kFusedBlocks * kFusedMaxNeurons;
 // LDS bytes the fused kernel may spend on the staged x rows.
 constexpr int kXLdsBytes = 128 * 1024;

@@ -49,7 +49,7 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
   constexpr int W = kFusedWaves;
   constexpr int NT = W * kWaveSize;
   constexpr int QMAX = (NCH + W - 1) / W;  // down-stage chunks per wave
-  constexpr int RB = 8;                    // down rows per batch
+  constexpr int RB = QMAX >= 4 ? 2 : 8 / QMAX;  // down rows per batch
   constexpr int NBMAX = kFusedMaxNeurons;  // neurons per block
 
   __shared__ __attribute__((aligned(16))) float xs[BT * DP];

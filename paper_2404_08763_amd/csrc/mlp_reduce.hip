@@ -11,6 +11,7 @@ constexpr int kReduceThreads = 256;
 constexpr int kReduceCols4 = 8;                             // float4 columns per block
 constexpr int kReduceSubs = kReduceThreads / kReduceCols4;  // partial subsets per block
 constexpr int kReducePer = kFusedBlocks / kReduceSubs;      // partials per thread
+static_assert(kFusedBlocks % kReduceSubs == 0, "partials must split evenly over the subsets");
 
 __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
   const int tid = threadIdx.x;
@@ -61,16 +62,15 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
   // the ascending list.
   __shared__ int offs[kFusedBlocks + 1];
   const int b = blockIdx.x - nred;
-  const int g = tid;
-  int base = 0, sc = 0, mine = 0;
-  if (g < a.G) {
-    base = (int)(((int64_t)g * a.m) / a.G);
-    sc = a.seg_cnt[g];
+  for (int g = tid; g < a.G; g += kReduceThreads) {
+    const int base = (int)(((int64_t)g * a.m) / a.G);
+    const int sc = a.seg_cnt[g];
+    int mine = 0;
     for (int e = 0; e < sc; ++e) mine += (int)((a.seg_mask[base + e] >> b) & 1u);
+    offs[g] = mine;
   }
-  offs[g] = mine;
   __syncthreads();
-  if (tid == 0) {  // exclusive scan over at most 256 segment counts
+  if (tid == 0) {  // exclusive scan over the segment counts
     int run = 0;
     for (int k = 0; k < a.G; ++k) {
       const int c = offs[k];
@@ -80,7 +80,9 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
     offs[a.G] = run;
   }
   __syncthreads();
-  if (g < a.G) {
+  for (int g = tid; g < a.G; g += kReduceThreads) {
+    const int base = (int)(((int64_t)g * a.m) / a.G);
+    const int sc = a.seg_cnt[g];
     int pos = offs[g];
     for (int e = 0; e < sc; ++e) {
       if ((a.seg_mask[base + e] >> b) & 1u) {
