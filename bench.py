@@ -48,6 +48,9 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="only the timed region (for profilers)")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="after the timed region, one device-to-device copy of this many MiB "
+                         "(a plain copy of known size that scales hardware byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -164,6 +167,16 @@ def main() -> int:
             "weight_copies_rotated": R, "decode_vectors": ntok,
         },
     }
+
+    if args.copy_probe_mb > 0:
+        nb = args.copy_probe_mb << 20
+        src = torch.ones(nb // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_probe_bytes"] = nb
+        del src, dst
 
     if not args.no_extras:
         per_k = {}

@@ -4,14 +4,14 @@
  *
  * The operations follow Lee et al., "CATS: Contextually-Aware Thresholding
  * for Sparsity in Large Language Models" (COLM 2024):
- *   Section 2, Eq. 1   Gated-MLP(x) = (SiLU(x W_gate) * (x W_up)) W_down,
+ *   Section 3, Eq. 1   Gated-MLP(x) = (SiLU(x W_gate) * (x W_up)) W_down,
  *                      x in R^{b x d}, W_gate, W_up in R^{d x m},
  *                      W_down in R^{m x d}
- *   Section 2, Eq. 2   SiLU(z) = z / (1 + e^{-z})
- *   Section 3.1, Eq. 3 cutoff t = min{t' : F(t') >= k}, F the empirical CDF
+ *   Section 3, Eq. 2   SiLU(z) = z / (1 + e^{-z})
+ *   Section 4.1, Eq. 3 cutoff t = min{t' : F(t') >= k}, F the empirical CDF
  *                      of the absolute gate activations of one MLP block
- *   Section 3.2, Eq. 4-5  CATS_t keeps an activation when |.| >= t
- *   Section 3.3 and Appendix D  kernel algorithms "MLP using CATS"
+ *   Section 4.2, Eq. 4-5  CATS_t keeps an activation when |.| >= t
+ *   Section 4.3 and Appendix D  kernel algorithms "MLP using CATS"
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -92,7 +92,7 @@ typedef struct {
  *   active_cnt[b]        number of kept neurons
  *   active_v[b*m + q]    its activation v = SiLU(x W_gate[:, j]) (Eq. 2)
  *   active_h[b*m + q]    v * (x W_up[:, j]), the x1 of the CATS kernel
- *                        algorithm (Section 3.3), before W_down
+ *                        algorithm (Section 4.3), before W_down
  * Entries past active_cnt[b] are left untouched.  All dev, int32 / fp32. */
 typedef struct {
   int32_t* active_idx;
@@ -120,12 +120,12 @@ size_t cats_workspace_bytes(int32_t d, int32_t m, int32_t max_batch, int64_t max
 /* Transpose a row-major [rows x cols] matrix into [cols x rows]
  * (w_t[c*rows + r] = w[r*cols + c]), bit for bit.  Used to turn the math
  * layout W_gate, W_up [d x m] of Eq. 1 into the neuron-major [m x d]
- * the kernels stream (Section 3.3 stores W_up this way so that a masked
+ * the kernels stream (Section 4.3 stores W_up this way so that a masked
  * neuron's weights are one contiguous row).  dev w, dev w_t, no overlap. */
 cats_status cats_pack_weights(const void* w, void* w_t, int32_t rows, int32_t cols,
                               int32_t dtype, void* stream);
 
-/* Calibration activations (Section 3.1): for N vectors x_n (dev [N x d],
+/* Calibration activations (Section 4.1): for N vectors x_n (dev [N x d],
  * fp32) writes acts[n*m + j] = |SiLU(x_n . W_gate[:, j])| (dev [N x m]).
  * Enqueue only. */
 cats_status cats_calib_activations(const cats_layer* layer, const float* x, int32_t N,
@@ -140,7 +140,7 @@ cats_status cats_calib_activations(const cats_layer* layer, const float* x, int3
 cats_status cats_threshold_from_acts(const float* acts, int64_t n, double sparsity,
                                      void* ws, size_t ws_bytes, void* stream, float* t_out);
 
-/* Per-block cutoff calibration (Section 3.1, Eq. 3): activations of the N
+/* Per-block cutoff calibration (Section 4.1, Eq. 3): activations of the N
  * calibration vectors (dev [N x d], fp32) through the gate, pooled over
  * all N*m values, then cats_threshold_from_acts.  *t_out is host.
  * Synchronises `stream`.  Needs max_calib_values >= N*m in the workspace. */
@@ -149,7 +149,7 @@ cats_status cats_calibrate_threshold(const cats_layer* layer, const float* calib
                                      float* t_out);
 
 /* CATS MLP forward (Eq. 1 with the CATS_t activation of Eq. 5; the
- * "MLP using CATS" algorithm of Section 3.3):
+ * "MLP using CATS" algorithm of Section 4.3):
  *   v = SiLU(x W_gate); Mask = |v| >= t; x1 = (x W_up[Mask]) * v[Mask];
  *   y = residual + x1 W_down[Mask]
  * for B rows x (dev [B x d]); y (dev [B x d]); residual dev [B x d] or
@@ -162,7 +162,7 @@ cats_status cats_mlp_forward(const cats_layer* layer, const float* x, int32_t B,
                              void* ws, size_t ws_bytes, void* stream);
 
 /* Dense gated MLP (Eq. 1, every neuron kept): the comparison baseline
- * ("Dense" of Section 4.3).  Same arguments and layouts as the forward. */
+ * ("Dense" of Section 5.3).  Same arguments and layouts as the forward. */
 cats_status cats_mlp_dense(const cats_layer* layer, const float* x, int32_t B,
                            const float* residual, float* y, void* ws, size_t ws_bytes,
                            void* stream);

@@ -1,7 +1,7 @@
 """CATS CPU oracle -- TEST INFRASTRUCTURE ONLY.
 
 A plain, sequential C implementation of the CATS gated MLP (Eq. 1-5 and the
-"MLP using CATS" kernel algorithm of Section 3.3) and of the cutoff
+"MLP using CATS" kernel algorithm of Section 4.3) and of the cutoff
 calibration (Eq. 3), loaded through ctypes.  Only ``tests/``,
 ``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may use
 it; the product library never does, and it shares no code with it.

@@ -6,7 +6,7 @@
  *   Eq. 2  SiLU(z) = z * sigmoid(z) = z / (1 + e^{-z})
  *   Eq. 3  t = min{t' : F(t') >= k}, F the empirical CDF of |activations|
  *   Eq. 4/5 CATS_t keeps an activation when |.| >= t, else zeroes it
- *   Section 3.3, "MLP using CATS": v = SiLU(x W_gate); Mask = |v| >= t;
+ *   Section 4.3, "MLP using CATS": v = SiLU(x W_gate); Mask = |v| >= t;
  *          x1 = (x W_up[Mask]) * v[Mask]; y = x1 W_down[Mask]
  * Nothing here is blocked, fused or reordered beyond those definitions:
  * every sum runs over its index in ascending order starting from +0.

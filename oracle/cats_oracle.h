@@ -8,13 +8,13 @@
  * product path (libcats) never links or calls it, and the two share no
  * code, header or helper.
  *
- * Precision: the paper runs all experiments in FP32 (Section 4, setup), so
+ * Precision: the paper runs all experiments in FP32 (Section 5, setup), so
  * the default build accumulates in float with a strictly ascending index
  * order and no fused multiply-add (-O2 -ffp-contract=off, no fast-math).
  * Building with -DORACLE_F64 gives the same code in double, which bounds
  * the float build's own rounding.
  *
- * Layouts follow the paper's notation (Section 2, Eq. 1):
+ * Layouts follow the paper's notation (Section 3, Eq. 1):
  *   x       [B x d]   row-major
  *   w_gate  [d x m]   row-major (math layout, element (i,j) at i*m + j)
  *   w_up    [d x m]   row-major
@@ -37,7 +37,7 @@ const char* oracle_precision(void);
 double oracle_silu(double z);
 
 /* The gated MLP with the CATS activation (Eq. 1 with Eq. 5, and the
- * "MLP using CATS" algorithm of Section 3.3).  For every row b:
+ * "MLP using CATS" algorithm of Section 4.3).  For every row b:
  *   g_j = sum_i x_bi Wg[i,j],  u_j = sum_i x_bi Wu[i,j]   (ascending i)
  *   v_j = SiLU(g_j)
  *   neuron j is active when |v_j| >= t   (written !(|v_j| < t); Eq. 4)
@@ -59,7 +59,7 @@ int oracle_cats_mlp(const float* x, int32_t B, int32_t d, int32_t m,
  * the sum of squares taken in ascending i. */
 int oracle_rmsnorm(const float* x, int32_t B, int32_t d, double eps, double* out);
 
-/* Calibration activations (Section 3.1): a[n*m + j] = |SiLU(x_n . Wg[:,j])|
+/* Calibration activations (Section 4.1): a[n*m + j] = |SiLU(x_n . Wg[:,j])|
  * for N calibration vectors. */
 int oracle_calib_acts(const float* X, int32_t N, int32_t d, int32_t m,
                       const float* w_gate, double* acts);

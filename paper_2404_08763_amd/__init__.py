@@ -3,7 +3,7 @@
 CATS (Contextually-Aware Thresholding for Sparsity, Lee et al., COLM 2024)
 wraps the SiLU of a gated MLP in a magnitude cutoff t calibrated per block
 (Eq. 3-5) and then reads only the W_up / W_down rows of the neurons that
-survive (Section 3.3).  The work runs in hand-written HIP kernels inside
+survive (Section 4.3).  The work runs in hand-written HIP kernels inside
 libcats.so behind a C ABI (include/cats.h); this package is its ctypes
 binding.  Build with ``python -m paper_2404_08763_amd.build``.
 """

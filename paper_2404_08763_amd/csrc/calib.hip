@@ -1,4 +1,4 @@
-// Cutoff calibration (Section 3.1, Eq. 3).
+// Cutoff calibration (Section 4.1, Eq. 3).
 //
 // 1. k_calib_acts: the activations the cutoff is a percentile of,
 //    a[n, j] = |SiLU(x_n . W_gate[:, j])|, for N calibration vectors: a

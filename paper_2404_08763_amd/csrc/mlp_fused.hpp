@@ -3,7 +3,7 @@
 // down-projection into per-block partial sums, in one pass over the weights.
 //
 // Method (Eq. 1, Eq. 2, Eq. 5 and the "MLP using CATS" algorithm of
-// Section 3.3 / Appendix D):
+// Section 4.3 / Appendix D):
 //   v_j = SiLU(x . W_gate[:, j]);  neuron j is active when |v_j| >= t
 //   h_j = v_j * (x . W_up[:, j])            only for active j
 //   y  += h_j * W_down[j, :]                only for active j

@@ -5,7 +5,7 @@ drawn from seeded CPU generators, with no part of the method's arithmetic.
 Both the device path and the CPU oracle are fed from these buffers.
 
 The paper times single Llama2-7B (d=4096, m=11008) and Mistral-7B (d=4096,
-m=14336) MLP blocks with real weights and RefinedWeb tokens (Section 4.3);
+m=14336) MLP blocks with real weights and RefinedWeb tokens (Section 5.3);
 neither is available here, so weights are N(0, 0.02^2) and activations are
 synthetic with the distributions below.
 
