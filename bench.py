@@ -37,6 +37,27 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def fused_traffic(cfg_name):
+    """HBM bytes per fused-kernel launch from the committed byte-counter record,
+    or None when there is none for this workload or when any source the kernel
+    is built from has changed since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"mlp_fused_{cfg_name}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    h = hashlib.sha256()
+    for src in rec["sources"]:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec["source_sha256"]:
+        return None
+    per = [v["read_bytes"] + v["write_bytes"] for v in rec["per_k"].values()]
+    return int(sum(per) / len(per))
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -212,7 +233,7 @@ def main() -> int:
         out["roofline"] = {
             "kernel": "k_mlp_fused (CATS)", "bound": "hbm", "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": None, "avg_launch_us": round(avg_us, 3), "launches": n_launch,
+            "traffic": fused_traffic(cfg.name), "avg_launch_us": round(avg_us, 3), "launches": n_launch,
             "bytes_per_launch": int(k1_total / max(1, n_launch)),
         }
         out["kernel_avg_us"] = {n: round(v[1] * 1e3 / max(1, v[0]), 3) for n, v in kt.items()}

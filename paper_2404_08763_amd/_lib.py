@@ -165,11 +165,11 @@ def workspace_bytes(d: int, m: int, max_batch: int = 1, max_calib_values: int = 
 
 
 def workspace(d: int, m: int, max_batch: int = 1, max_calib_values: int = 0, device="cuda") -> torch.Tensor:
-    """A device byte buffer of cats_workspace_bytes(...) bytes."""
+    """A zero-filled device byte buffer of cats_workspace_bytes(...) bytes."""
     n = workspace_bytes(d, m, max_batch, max_calib_values)
     if n == 0:
         raise ValueError("arguments outside the supported range")
-    ws = torch.empty(n, dtype=torch.uint8, device=device)
+    ws = torch.zeros(n, dtype=torch.uint8, device=device)
     assert ws.data_ptr() % 256 == 0
     return ws
 

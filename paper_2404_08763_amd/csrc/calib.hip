@@ -107,11 +107,11 @@ hipError_t launch_calib_acts(int wdtype_bf16, const float* x, const void* wg_t, 
   const dim3 grid((m + kCalibTN - 1) / kCalibTN, (N + kCalibTM - 1) / kCalibTM);
   KernelTimer timer("calib_acts", s);
   if (wdtype_bf16)
-    hipLaunchKernelGGL(k_calib_acts<wbf16>, grid, dim3(256), 0, s, x,
-                       static_cast<const uint16_t*>(wg_t), N, d, m, acts);
+    hipExtLaunchKernelGGL(k_calib_acts<wbf16>, grid, dim3(256), 0, s, timer.start(), timer.stop(), 0,
+                          x, static_cast<const uint16_t*>(wg_t), N, d, m, acts);
   else
-    hipLaunchKernelGGL(k_calib_acts<wf32>, grid, dim3(256), 0, s, x,
-                       static_cast<const float*>(wg_t), N, d, m, acts);
+    hipExtLaunchKernelGGL(k_calib_acts<wf32>, grid, dim3(256), 0, s, timer.start(), timer.stop(), 0,
+                          x, static_cast<const float*>(wg_t), N, d, m, acts);
   return hipGetLastError();
 }
 
@@ -179,19 +179,22 @@ hipError_t launch_radix_select(const float* a, int64_t n, int64_t r, uint32_t* s
   if (blocks < 1) blocks = 1;
   {
     KernelTimer timer("radix_init", s);
-    hipLaunchKernelGGL(k_radix_init, dim3(1), dim3(256), 0, s, scratch, (uint64_t)r);
+    hipExtLaunchKernelGGL(k_radix_init, dim3(1), dim3(256), 0, s, timer.start(), timer.stop(), 0,
+                          scratch, (uint64_t)r);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   for (int pass = 0; pass < 4; ++pass) {
     {
       KernelTimer timer("radix_hist", s);
-      hipLaunchKernelGGL(k_radix_hist, dim3((unsigned)blocks), dim3(256), 0, s, a, n, scratch, pass);
+      hipExtLaunchKernelGGL(k_radix_hist, dim3((unsigned)blocks), dim3(256), 0, s, timer.start(),
+                            timer.stop(), 0, a, n, scratch, pass);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     {
       KernelTimer timer("radix_pick", s);
-      hipLaunchKernelGGL(k_radix_pick, dim3(1), dim3(256), 0, s, scratch, pass);
+      hipExtLaunchKernelGGL(k_radix_pick, dim3(1), dim3(256), 0, s, timer.start(), timer.stop(), 0,
+                            scratch, pass);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }

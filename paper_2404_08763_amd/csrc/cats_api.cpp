@@ -305,7 +305,7 @@ int fused_bt_max(int wdtype_bf16, int nch) {
 
 int fused_grid(int m) { return m < kFusedBlocks ? m : kFusedBlocks; }
 
-KernelTimer::KernelTimer(const char* name, hipStream_t s) : slot_(-1), s_(s) {
+KernelTimer::KernelTimer(const char* name, hipStream_t) {
   TimerState& T = timer_state();
   std::lock_guard<std::mutex> lk(T.mu);
   if (!T.on) return;
@@ -315,16 +315,9 @@ KernelTimer::KernelTimer(const char* name, hipStream_t s) : slot_(-1), s_(s) {
   p.a = timer_event_locked(T);
   p.b = timer_event_locked(T);
   if (!p.a || !p.b) return;
-  if (hipEventRecord(p.a, s) != hipSuccess) return;
   T.pending.push_back(p);
-  slot_ = (int)T.pending.size() - 1;
-}
-
-KernelTimer::~KernelTimer() {
-  if (slot_ < 0) return;
-  TimerState& T = timer_state();
-  std::lock_guard<std::mutex> lk(T.mu);
-  if (slot_ < (int)T.pending.size()) (void)hipEventRecord(T.pending[slot_].b, s_);
+  a_ = p.a;
+  b_ = p.b;
 }
 
 }  // namespace cats

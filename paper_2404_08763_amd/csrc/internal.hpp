@@ -2,6 +2,7 @@
 // translation units.  Every launcher assumes its arguments were validated.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -91,16 +92,18 @@ hipError_t launch_rmsnorm(const float* x, float* xn, int B, int d, float eps, hi
 hipError_t launch_transpose(const void* in, void* out, int rows, int cols, int elem_bytes,
                             hipStream_t s);
 
-// Optional per-kernel timing (cats_timer_*): a scope that records HIP events
-// around one launch on its stream while the timer is enabled.
+// Optional per-kernel timing (cats_timer_*): while the timer is enabled a
+// KernelTimer hands out a pair of HIP events that the launch (through
+// hipExtLaunchKernelGGL) records at the kernel's own start and end; both
+// are null otherwise.
 class KernelTimer {
  public:
   KernelTimer(const char* name, hipStream_t s);
-  ~KernelTimer();
+  hipEvent_t start() const { return a_; }
+  hipEvent_t stop() const { return b_; }
 
  private:
-  int slot_;
-  hipStream_t s_;
+  hipEvent_t a_ = nullptr, b_ = nullptr;
 };
 
 }  // namespace cats

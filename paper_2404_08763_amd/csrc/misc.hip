@@ -26,7 +26,8 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ x, fl
 
 hipError_t launch_rmsnorm(const float* x, float* xn, int B, int d, float eps, hipStream_t s) {
   KernelTimer timer("rmsnorm", s);
-  hipLaunchKernelGGL(k_rmsnorm, dim3(B), dim3(256), 0, s, x, xn, d, eps);
+  hipExtLaunchKernelGGL(k_rmsnorm, dim3(B), dim3(256), 0, s, timer.start(), timer.stop(), 0, x, xn, d,
+                        eps);
   return hipGetLastError();
 }
 
@@ -53,11 +54,11 @@ hipError_t launch_transpose(const void* in, void* out, int rows, int cols, int e
   const dim3 grid((cols + 31) / 32, (rows + 31) / 32);
   KernelTimer timer("transpose", s);
   if (elem_bytes == 2)
-    hipLaunchKernelGGL(k_transpose<uint16_t>, grid, dim3(256), 0, s,
-                       static_cast<const uint16_t*>(in), static_cast<uint16_t*>(out), rows, cols);
+    hipExtLaunchKernelGGL(k_transpose<uint16_t>, grid, dim3(256), 0, s, timer.start(), timer.stop(), 0,
+                          static_cast<const uint16_t*>(in), static_cast<uint16_t*>(out), rows, cols);
   else
-    hipLaunchKernelGGL(k_transpose<uint32_t>, grid, dim3(256), 0, s,
-                       static_cast<const uint32_t*>(in), static_cast<uint32_t*>(out), rows, cols);
+    hipExtLaunchKernelGGL(k_transpose<uint32_t>, grid, dim3(256), 0, s, timer.start(), timer.stop(), 0,
+                          static_cast<const uint32_t*>(in), static_cast<uint32_t*>(out), rows, cols);
   return hipGetLastError();
 }
 

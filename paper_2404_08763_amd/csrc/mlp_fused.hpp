@@ -339,17 +339,17 @@ hipError_t launch_fused_nch(int bt, const FusedArgs& a, int G, hipStream_t s) {
   const dim3 grid(G), block(kFusedWaves * kWaveSize);
   KernelTimer timer(DENSE ? "mlp_fused_dense" : "mlp_fused_cats", s);
   switch (bt) {
-    case 1: hipLaunchKernelGGL((k_mlp_fused<WT, NCH, 1, DENSE, AUX>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((k_mlp_fused<WT, NCH, 2, DENSE, AUX>), grid, block, 0, s, a); break;
+    case 1: hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 1, DENSE, AUX>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
+    case 2: hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 2, DENSE, AUX>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
     case 4:
       if constexpr (4 * DP * 4 <= kXLdsBytes) {
-        hipLaunchKernelGGL((k_mlp_fused<WT, NCH, 4, DENSE, AUX>), grid, block, 0, s, a);
+        hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 4, DENSE, AUX>), grid, block, 0, s, timer.start(), timer.stop(), 0, a);
         break;
       }
       return hipErrorInvalidValue;
     case 8:
       if constexpr (8 * DP * 4 <= kXLdsBytes) {
-        hipLaunchKernelGGL((k_mlp_fused<WT, NCH, 8, DENSE, AUX>), grid, block, 0, s, a);
+        hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 8, DENSE, AUX>), grid, block, 0, s, timer.start(), timer.stop(), 0, a);
         break;
       }
       return hipErrorInvalidValue;

@@ -102,7 +102,8 @@ hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s) {
   const int ncb = (d4 + kReduceCols4 - 1) / kReduceCols4;
   const int grid = a.B * ncb + (a.aux ? a.B : 0);
   KernelTimer timer("k_mlp_reduce", s);
-  hipLaunchKernelGGL(k_mlp_reduce, dim3(grid), dim3(kReduceThreads), 0, s, a);
+  hipExtLaunchKernelGGL(k_mlp_reduce, dim3(grid), dim3(kReduceThreads), 0, s, timer.start(), timer.stop(), 0,
+                        a);
   return hipGetLastError();
 }
 

@@ -142,10 +142,13 @@ def test_batch_rows_have_their_own_masks(dev, oracle32, B):
     # rows differ in their masks (contextual sparsity)
     cnt = aux["cnt"].cpu().numpy()
     assert len(set(cnt.tolist())) > 1 or B == 1
-    # each row equals its own batch-1 call bit for bit
+    # each row equals its own batch-1 call up to summation order (the down
+    # projection spreads the batch's union list over the lanes, so a row's
+    # terms are grouped differently when other rows share the call)
     for b in range(B):
         yb = P.mlp_forward(layer, x[b : b + 1].cuda(), t, residual=res[b : b + 1].cuda())
-        assert torch.equal(yb.view(torch.int32), y[b : b + 1].view(torch.int32))
+        scale = float(y[b].abs().max())
+        assert float((yb[0] - y[b]).abs().max()) <= 1e-5 * scale
 
 
 # ------------------------------------------------------ edge cases (C1 size)
@@ -192,6 +195,30 @@ def test_determinism_and_aux_invariance(c1):
             for b in range(8):
                 n = int(a1["cnt"][b])
                 assert torch.equal(a1[k][b, :n], a2[k][b, :n])
+
+
+def test_shared_workspace_across_shapes(dev, oracle32):
+    """One workspace, filled with garbage first, serves calls of different
+    shapes and batch sizes in a row (nothing a call needs is left over from
+    the previous one)."""
+    shapes = [(4096, 11008, 1), (256, 688, 3), (1032, 7, 2), (5120, 300, 4), (4096, 11008, 1)]
+    nbytes = max(P.workspace_bytes(d, m, B, 0) for d, m, B in shapes)
+    ws = torch.full((nbytes,), 0xAB, dtype=torch.uint8, device=dev)
+    for i, (d, m, B) in enumerate(shapes):
+        say("shared workspace", i, d, m, B)
+        g = torch.Generator().manual_seed(300 + i)
+        wg, wu, wd = [(torch.randn(sh, generator=g) * 0.02).to(torch.bfloat16)
+                      for sh in ((d, m), (d, m), (m, d))]
+        x = torch.randn((B, d), generator=g)
+        layer = device_layer(wg, wu, wd)
+        hw = host_f32(wg, wu, wd)
+        ref_all = oracle32.cats_mlp(x.numpy(), *hw, t=0.0)
+        t = quantile_t(np.abs(ref_all["v"]), 0.6)
+        ref = oracle32.cats_mlp(x.numpy(), *hw, t=t)
+        ys = [P.mlp_forward(layer, x.cuda(), t, ws=ws) for _ in range(3)]
+        for y in ys[1:]:
+            assert torch.equal(ys[0].view(torch.int32), y.view(torch.int32))
+        check_forward(ys[0], None, ref, t, B, f"shared ws {d}x{m} B={B}")
 
 
 def test_rmsnorm(dev, oracle32):
