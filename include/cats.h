@@ -71,6 +71,8 @@ typedef enum { CATS_F32 = 0, CATS_BF16 = 1 } cats_dtype;
 #define CATS_MAX_M 65536
 #define CATS_MAX_D_F32 4096
 #define CATS_MAX_BATCH 16
+/* Layers of one cats_stack_forward call. */
+#define CATS_MAX_LAYERS 1024
 /* Each weight matrix (m * d elements) is addressed with 32-bit offsets and
  * may span at most 1 GiB. */
 #define CATS_MAX_MATRIX_BYTES (1ull << 30)
@@ -111,7 +113,7 @@ const char* cats_status_string(cats_status s);
 const char* cats_last_error(void);
 
 /* Workspace bytes needed by any call on a block of size d x m with up to
- * `max_batch` rows per forward/dense call and up to `max_calib_values`
+ * `max_batch` rows per forward, dense or stack call and up to `max_calib_values`
  * calibration activations (N * m) per calibration call (0 if calibration
  * is not used).  Pure host arithmetic, no HIP call.  Returns 0 for
  * arguments outside the supported range. */
@@ -166,6 +168,45 @@ cats_status cats_mlp_forward(const cats_layer* layer, const float* x, int32_t B,
 cats_status cats_mlp_dense(const cats_layer* layer, const float* x, int32_t B,
                            const float* residual, float* y, void* ws, size_t ws_bytes,
                            void* stream);
+
+/* Residual stack of CATS MLP blocks: the MLP half of a decoder's decode
+ * step, with the attention sub-layers left out (the paper sparsifies only
+ * the MLP blocks, Section 4; norms and residuals are outside its formulas,
+ * Appendix B).  For l = 0 .. L-1:
+ *   x_{l+1} = x_l + MLP_l(RMSNorm(x_l))
+ * with unit-gain RMSNorm of epsilon eps (computed inside the fused kernel)
+ * and MLP_l the CATS forward of layers[l] at threshold t[l] (host array of
+ * L values, each >= 0), or the dense MLP for every layer when t is NULL.
+ *   layers   host array of L blocks (1 <= L <= CATS_MAX_LAYERS), one d for
+ *            all; m may differ per layer
+ *   x0       dev [B x d] fp32, the residual stream entering layer 0
+ *   x_out    dev [B x d] fp32, receives x_L; must not overlap x0 or ws
+ *   x_all    dev [(L+1) x B x d] fp32 or NULL; receives every x_l
+ *            (x_all[0] = x0)
+ *   aux      host array of L cats_forward_aux (layer l's outputs for its
+ *            MLP, as in cats_mlp_forward) or NULL; needs t
+ * Workspace: cats_workspace_bytes(d, the largest m, B, 0).  Enqueue only;
+ * two launches per layer on `stream`. */
+cats_status cats_stack_forward(const cats_layer* layers, int32_t L, const float* t,
+                               const float* x0, int32_t B, float eps, float* x_out,
+                               float* x_all, const cats_forward_aux* aux, void* ws,
+                               size_t ws_bytes, void* stream);
+
+/* Per-block cutoffs of a stack (Eq. 3 for every block, Section 4.1): the
+ * N calibration vectors (dev [N x d] fp32, the residual stream entering
+ * layer 0) are propagated through the stack densely, as the thresholds
+ * are set on the unsparsified model, and block l's threshold is calibrated
+ * on what it sees, RMSNorm(x_l) with epsilon eps:
+ *   t_out[l] = cats_calibrate_threshold(layer l, RMSNorm(x_l), sparsity)
+ *   x_{l+1}  = x_l + dense MLP_l(RMSNorm(x_l))
+ * t_out is a host array of L floats.  k = 0 gives t = 0 for every layer
+ * without touching the device.  Workspace:
+ * cats_calibrate_stack_workspace_bytes(d, largest m, N).  Synchronises
+ * `stream` (once per layer).  Offline. */
+size_t cats_calibrate_stack_workspace_bytes(int32_t d, int32_t max_m, int32_t N);
+cats_status cats_calibrate_stack(const cats_layer* layers, int32_t L, const float* calib_x,
+                                 int32_t N, double sparsity, float eps, void* ws,
+                                 size_t ws_bytes, void* stream, float* t_out);
 
 /* RMSNorm with unit gain, xn = x / sqrt(mean(x^2) + eps), rows of d fp32
  * (dev [B x d]); the normalisation in front of each MLP block of a

@@ -74,6 +74,10 @@ class Oracle:
         L.oracle_cats_mlp.restype = ctypes.c_int
         L.oracle_rmsnorm.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _PD]
         L.oracle_rmsnorm.restype = ctypes.c_int
+        _PPF = ctypes.POINTER(_PF)
+        L.oracle_stack.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                   _PPF, _PPF, _PPF, _PD, ctypes.c_int32, ctypes.c_double, _PF, _PI]
+        L.oracle_stack.restype = ctypes.c_int
         L.oracle_calib_acts.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _PF, _PD]
         L.oracle_calib_acts.restype = ctypes.c_int
         L.oracle_calib_acts_at.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -132,6 +136,36 @@ class Oracle:
         if self._L.oracle_rmsnorm(_ptr(x, _PF), x.shape[0], x.shape[1], float(eps), _ptr(out, _PD)) != 0:
             raise ValueError("oracle_rmsnorm rejected its arguments")
         return out
+
+    def stack(self, x0, layers, ts=None, eps=1e-5):
+        """Residual stack x_{l+1} = x_l + MLP_l(RMSNorm(x_l)) (see the header).
+
+        layers: list of (w_gate [d, m], w_up [d, m], w_down [m, d]) host
+        arrays; ts: one threshold per layer, or None for the dense stack.
+        Returns (x_all [(L+1), B, d] float32, active counts [L, B])."""
+        x0 = np.ascontiguousarray(x0, dtype=_F)
+        if x0.ndim == 1:
+            x0 = x0[None, :]
+        B, d = x0.shape
+        L = len(layers)
+        ws = [[np.ascontiguousarray(w, dtype=_F) for w in lw] for lw in layers]
+        m = ws[0][0].shape[1] if L else 1
+        for wg, wu, wd in ws:
+            assert wg.shape == (d, m) and wu.shape == (d, m) and wd.shape == (m, d)
+        PP = _PF * max(L, 1)
+        pg = PP(*[w[0].ctypes.data_as(_PF) for w in ws])
+        pu = PP(*[w[1].ctypes.data_as(_PF) for w in ws])
+        pd = PP(*[w[2].ctypes.data_as(_PF) for w in ws])
+        dense = ts is None
+        tarr = None if dense else np.ascontiguousarray(ts, dtype=np.float64)
+        assert dense or tarr.shape == (L,)
+        x_all = np.empty((L + 1, B, d), _F)
+        cnt = np.empty((max(L, 1), B), np.int32)
+        rc = self._L.oracle_stack(_ptr(x0, _PF), B, d, m, L, pg, pu, pd, _ptr(tarr, _PD), int(dense),
+                                  float(eps), _ptr(x_all, _PF), _ptr(cnt, _PI))
+        if rc != 0:
+            raise ValueError("oracle_stack rejected its arguments")
+        return x_all, cnt[:L].copy()
 
     def calib_acts(self, X, w_gate):
         X = np.ascontiguousarray(X, dtype=_F)

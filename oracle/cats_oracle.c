@@ -116,6 +116,39 @@ int oracle_rmsnorm(const float* x, int32_t B, int32_t d, double eps, double* out
   return 0;
 }
 
+int oracle_stack(const float* x0, int32_t B, int32_t d, int32_t m, int32_t L,
+                 const float* const* w_gate, const float* const* w_up,
+                 const float* const* w_down, const double* t, int32_t dense, double eps,
+                 float* x_all, int32_t* active_cnt) {
+  if (!x0 || !w_gate || !w_up || !w_down || !x_all || B <= 0 || d <= 0 || m <= 0 || L < 0)
+    return -1;
+  if (!dense && !t) return -1;
+  const size_t n = (size_t)B * d;
+  double* tmp = (double*)malloc(sizeof(double) * n);
+  float* xn = (float*)malloc(sizeof(float) * n);
+  double* y = (double*)malloc(sizeof(double) * n);
+  int32_t* cnt = (int32_t*)malloc(sizeof(int32_t) * (size_t)B);
+  int rc = (tmp && xn && y && cnt) ? 0 : -1;
+  if (rc == 0) memcpy(x_all, x0, sizeof(float) * n);
+  for (int32_t l = 0; l < L && rc == 0; ++l) {
+    const float* xl = x_all + (size_t)l * n;
+    float* xnext = x_all + (size_t)(l + 1) * n;
+    rc = oracle_rmsnorm(xl, B, d, eps, tmp);
+    if (rc != 0) break;
+    for (size_t i = 0; i < n; ++i) xn[i] = (float)tmp[i];
+    rc = oracle_cats_mlp(xn, B, d, m, w_gate[l], w_up[l], w_down[l], dense ? 0.0 : t[l], dense, xl,
+                         y, NULL, cnt, NULL, NULL);
+    if (rc != 0) break;
+    for (size_t i = 0; i < n; ++i) xnext[i] = (float)y[i];
+    if (active_cnt) memcpy(active_cnt + (size_t)l * B, cnt, sizeof(int32_t) * (size_t)B);
+  }
+  free(tmp);
+  free(xn);
+  free(y);
+  free(cnt);
+  return rc;
+}
+
 /* |SiLU(x_n . Wg[:,j])|, the activation whose CDF defines the cutoff. */
 static real calib_act(const float* xn, int32_t d, int32_t m, const float* w_gate, int32_t j) {
   real g = 0;

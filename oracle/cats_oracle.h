@@ -59,6 +59,23 @@ int oracle_cats_mlp(const float* x, int32_t B, int32_t d, int32_t m,
  * the sum of squares taken in ascending i. */
 int oracle_rmsnorm(const float* x, int32_t B, int32_t d, double eps, double* out);
 
+/* Residual stack of L gated-MLP blocks, the MLP half of a decoder's layers
+ * (norms and residuals sit outside the paper's formulas, Appendix B).  For
+ * l = 0 .. L-1 and every row b:
+ *   xn      = RMSNorm(x_l)          unit gain, epsilon eps
+ *   x_{l+1} = x_l + MLP_l(xn)       MLP_l: oracle_cats_mlp at t[l], or
+ *                                   dense for every layer when dense != 0
+ * The residual stream is a float vector between layers: xn and x_{l+1} are
+ * stored as float (exact in the f32 build, rounded in the f64 build).
+ * w_gate[l], w_up[l], w_down[l] point at layer l's math-layout weights,
+ * every layer d x m.  x_all [(L+1) x B x d] receives x_0 .. x_L;
+ * active_cnt [L x B] (NULL to skip) the kept neurons of every layer and
+ * row.  Returns 0, or -1 on a bad argument. */
+int oracle_stack(const float* x0, int32_t B, int32_t d, int32_t m, int32_t L,
+                 const float* const* w_gate, const float* const* w_up,
+                 const float* const* w_down, const double* t, int32_t dense, double eps,
+                 float* x_all, int32_t* active_cnt);
+
 /* Calibration activations (Section 4.1): a[n*m + j] = |SiLU(x_n . Wg[:,j])|
  * for N calibration vectors. */
 int oracle_calib_acts(const float* X, int32_t N, int32_t d, int32_t m,

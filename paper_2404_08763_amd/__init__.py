@@ -20,7 +20,10 @@ from ._lib import (  # noqa: F401
     mlp_forward,
     pack_weights,
     raw,
+    Stack,
+    calibrate_stack,
     rmsnorm,
+    stack_forward,
     threshold_from_acts,
     timer_enable,
     timer_read,

@@ -65,6 +65,11 @@ _SIGNATURES = {
     "cats_mlp_forward": ([ctypes.POINTER(_Layer), _vp, _i32, _f32, _vp, _vp, ctypes.POINTER(_Aux),
                           _vp, _sz, _vp], _i32),
     "cats_mlp_dense": ([ctypes.POINTER(_Layer), _vp, _i32, _vp, _vp, _vp, _sz, _vp], _i32),
+    "cats_stack_forward": ([ctypes.POINTER(_Layer), _i32, ctypes.POINTER(_f32), _vp, _i32, _f32, _vp,
+                            _vp, ctypes.POINTER(_Aux), _vp, _sz, _vp], _i32),
+    "cats_calibrate_stack_workspace_bytes": ([_i32, _i32, _i32], _sz),
+    "cats_calibrate_stack": ([ctypes.POINTER(_Layer), _i32, _vp, _i32, _f64, _f32, _vp, _sz, _vp,
+                              ctypes.POINTER(_f32)], _i32),
     "cats_rmsnorm": ([_vp, _vp, _i32, _i32, _f32, _vp], _i32),
     "cats_timer_enable": ([_i32], _i32),
     "cats_timer_reset": ([], _i32),
@@ -277,6 +282,84 @@ def mlp_dense(layer: Layer, x: torch.Tensor, residual: Optional[torch.Tensor] = 
     _check(raw().cats_mlp_dense(layer.c, _ptr(x), B, _ptr(residual), _ptr(out), _ptr(ws), ws.numel(),
                                 _stream()))
     return out
+
+
+class Stack:
+    """L blocks with one d, marshalled once for repeated stack calls.
+
+    t: one threshold per layer, or None for the dense stack."""
+
+    def __init__(self, layers, t=None):
+        self.layers = list(layers)
+        L = len(self.layers)
+        if L == 0:
+            raise ValueError("a stack needs at least one layer")
+        self.d = self.layers[0].d
+        self.max_m = max(l.m for l in self.layers)
+        self._arr = (_Layer * L)(*[l._c for l in self.layers])
+        self._t = None
+        if t is not None:
+            if len(t) != L:
+                raise ValueError(f"{len(t)} thresholds for {L} layers")
+            self._t = (_f32 * L)(*[float(v) for v in t])
+
+    def __len__(self):
+        return len(self.layers)
+
+
+def stack_forward(stack: Stack, x0: torch.Tensor, eps: float = 1e-5, out: Optional[torch.Tensor] = None,
+                  ws: Optional[torch.Tensor] = None, keep_all: bool = False, aux: bool = False):
+    """x_{l+1} = x_l + MLP_l(RMSNorm(x_l)) over the stack's layers.
+
+    Returns x_L, or a dict with "out", "x_all" [(L+1), B, d] (keep_all) and
+    "aux" (a list of per-layer dicts as from mlp_forward, when aux=True)."""
+    _dev(x0, "x0", torch.float32)
+    B = _rows(x0)
+    L = len(stack)
+    if out is None:
+        out = torch.empty_like(x0)
+    _dev(out, "out", torch.float32)
+    if ws is None:
+        ws = workspace(stack.d, stack.max_m, B, device=x0.device)
+    x_all = torch.empty((L + 1,) + tuple(x0.shape), dtype=torch.float32, device=x0.device) if keep_all else None
+    aux_bufs = None
+    aux_c = None
+    if aux:
+        aux_bufs, cs = [], []
+        for l in stack.layers:
+            m = l.m
+            b = {
+                "idx": torch.empty((B, m), dtype=torch.int32, device=x0.device),
+                "cnt": torch.empty((B,), dtype=torch.int32, device=x0.device),
+                "v": torch.empty((B, m), dtype=torch.float32, device=x0.device),
+                "h": torch.empty((B, m), dtype=torch.float32, device=x0.device),
+            }
+            aux_bufs.append(b)
+            cs.append(_Aux(b["idx"].data_ptr(), b["cnt"].data_ptr(), b["v"].data_ptr(), b["h"].data_ptr()))
+        aux_c = (_Aux * L)(*cs)
+    _check(raw().cats_stack_forward(stack._arr, L, stack._t, _ptr(x0), B, float(eps), _ptr(out),
+                                    _ptr(x_all), aux_c, _ptr(ws), ws.numel(), _stream()))
+    if not keep_all and not aux:
+        return out
+    return {"out": out, "x_all": x_all, "aux": aux_bufs}
+
+
+def calibrate_stack(stack: Stack, calib_x: torch.Tensor, sparsity: float, eps: float = 1e-5,
+                    ws: Optional[torch.Tensor] = None) -> list:
+    """Per-layer thresholds of a stack, the calibration vectors propagated
+    densely through the earlier layers (cats_calibrate_stack)."""
+    _dev(calib_x, "calib_x", torch.float32)
+    N = _rows(calib_x)
+    L = len(stack)
+    if ws is None:
+        n = int(raw().cats_calibrate_stack_workspace_bytes(stack.d, stack.max_m, N))
+        if n == 0:
+            raise ValueError("arguments outside the supported range")
+        ws = torch.zeros(n, dtype=torch.uint8, device=calib_x.device)
+    t = (_f32 * L)()
+    _check(raw().cats_calibrate_stack(stack._arr, L, _ptr(calib_x), N, float(sparsity), float(eps),
+                                      _ptr(ws), ws.numel(), _stream(), t))
+    return [float(v) for v in t]
 
 
 def rmsnorm(x: torch.Tensor, eps: float = 1e-5, out: Optional[torch.Tensor] = None) -> torch.Tensor:

@@ -68,6 +68,10 @@ FwdLayout fwd_layout(int d, int m, int bp) {
   return L;
 }
 
+// Two [B x d] fp32 buffers a stack ping-pongs its residual stream through
+// (placed after the forward region of the largest layer).
+size_t stack_rows_bytes(int d, int B) { return 2 * round_up((size_t)B * d * sizeof(float), kAlign); }
+
 size_t calib_bytes(int64_t nvalues) {
   return radix_bytes() + round_up((size_t)nvalues * sizeof(float), kAlign);
 }
@@ -112,9 +116,10 @@ int batch_tile(int rows) {
 }
 
 // Shared body of forward and dense.
+// norm: x is RMSNorm'ed (unit gain, eps) inside the fused kernel first.
 cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, bool dense,
                     const float* residual, float* y, const cats_forward_aux* aux, void* ws,
-                    size_t ws_bytes, void* stream) {
+                    size_t ws_bytes, void* stream, bool norm = false, float eps = 0.f) {
   cats_status st = check_layer(L);
   if (st != CATS_OK) return st;
   if (!x || !y) return fail(CATS_ERR_NULL, "x or y is NULL");
@@ -134,7 +139,9 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
   const int bt_max = cats::fused_bt_max(bf16, nch);
   const int rows_per_pass = B < bt_max ? B : bt_max;
   const FwdLayout lay = fwd_layout(d, m, rows_per_pass);
-  st = check_ws(ws, ws_bytes, lay.end);
+  // the full cats_workspace_bytes(d, m, B, 0), stack rows included, so one
+  // size rule holds for every call
+  st = check_ws(ws, ws_bytes, lay.end + stack_rows_bytes(d, B));
   if (st != CATS_OK) return st;
 
   char* w = static_cast<char*>(ws);
@@ -151,6 +158,8 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
     fa.d = d;
     fa.m = m;
     fa.t = dense ? 0.f : t;
+    fa.norm = norm ? 1 : 0;
+    fa.eps = eps;
     fa.partial = reinterpret_cast<float*>(w + lay.partial);
     fa.aux = want_aux ? 1 : 0;
     fa.seg_j = reinterpret_cast<int*>(w + lay.seg_j);
@@ -348,7 +357,7 @@ size_t cats_workspace_bytes(int32_t d, int32_t m, int32_t max_batch, int64_t max
       max_batch > CATS_MAX_BATCH || max_calib_values < 0)
     return 0;
   const int bp = max_batch < kMaxBatchTile ? max_batch : kMaxBatchTile;
-  const size_t fwd = fwd_layout(d, m, bp).end;
+  const size_t fwd = fwd_layout(d, m, bp).end + stack_rows_bytes(d, max_batch);
   const size_t cal = calib_bytes(max_calib_values);
   return fwd > cal ? fwd : cal;
 }
@@ -433,6 +442,134 @@ cats_status cats_mlp_forward(const cats_layer* layer, const float* x, int32_t B,
 cats_status cats_mlp_dense(const cats_layer* layer, const float* x, int32_t B, const float* residual,
                            float* y, void* ws, size_t ws_bytes, void* stream) {
   return run_mlp(layer, x, B, 0.f, true, residual, y, nullptr, ws, ws_bytes, stream);
+}
+
+cats_status cats_stack_forward(const cats_layer* layers, int32_t L, const float* t, const float* x0,
+                               int32_t B, float eps, float* x_out, float* x_all,
+                               const cats_forward_aux* aux, void* ws, size_t ws_bytes,
+                               void* stream) {
+  if (!layers) return fail(CATS_ERR_NULL, "layers is NULL");
+  if (!x0 || !x_out) return fail(CATS_ERR_NULL, "x0 or x_out is NULL");
+  if (L < 1 || L > CATS_MAX_LAYERS) return fail(CATS_ERR_SHAPE, "L=%d outside [1, %d]", (int)L, CATS_MAX_LAYERS);
+  if (B < 1 || B > CATS_MAX_BATCH) return fail(CATS_ERR_SHAPE, "B=%d outside [1, %d]", (int)B, CATS_MAX_BATCH);
+  if (!std::isfinite(eps) || eps < 0.f) return fail(CATS_ERR_RANGE, "eps must be finite and >= 0");
+  if (!t && aux) return fail(CATS_ERR_RANGE, "aux outputs need thresholds (t is NULL: dense stack)");
+  if (!aligned(x0, 16) || !aligned(x_out, 16) || (x_all && !aligned(x_all, 16)))
+    return fail(CATS_ERR_ALIGN, "x0, x_out and x_all must be 16-byte aligned");
+  const int d = layers[0].d;
+  size_t fwd_end = 0;
+  for (int l = 0; l < L; ++l) {
+    cats_status st = check_layer(&layers[l]);
+    if (st != CATS_OK) return fail(st, "layer %d: %s", l, g_last_error.c_str());
+    if (layers[l].d != d) return fail(CATS_ERR_SHAPE, "layer %d has d=%d, layer 0 has d=%d", l, (int)layers[l].d, d);
+    if (t && (std::isnan(t[l]) || t[l] < 0.f)) return fail(CATS_ERR_RANGE, "t[%d] must be >= 0 (got %g)", l, (double)t[l]);
+    const int bf16 = layers[l].wdtype == CATS_BF16;
+    const int bt_max = cats::fused_bt_max(bf16, cats::fused_nch(bf16, d));
+    const size_t e = fwd_layout(d, layers[l].m, B < bt_max ? B : bt_max).end;
+    if (e > fwd_end) fwd_end = e;
+  }
+  const size_t rows = (size_t)B * d;
+  const char* xo = reinterpret_cast<const char*>(x_out);
+  const char* xi = reinterpret_cast<const char*>(x0);
+  if (xo < xi + rows * 4 && xi < xo + rows * 4) return fail(CATS_ERR_RANGE, "x_out overlaps x0");
+  cats_status st = check_ws(ws, ws_bytes, fwd_end + stack_rows_bytes(d, B));
+  if (st != CATS_OK) return st;
+
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  float* pp[2] = {reinterpret_cast<float*>(static_cast<char*>(ws) + fwd_end),
+                  reinterpret_cast<float*>(static_cast<char*>(ws) + fwd_end +
+                                           round_up(rows * sizeof(float), kAlign))};
+  if (x_all) {
+    hipError_t e = hipMemcpyAsync(x_all, x0, rows * sizeof(float), hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "x_all[0] copy");
+  }
+  const float* cur = x0;
+  for (int l = 0; l < L; ++l) {
+    // the layer's output: x_all[l+1] when kept, the caller's x_out for the
+    // last layer, otherwise the ping-pong buffer cur does not occupy
+    float* dst = x_all ? x_all + (size_t)(l + 1) * rows : (l == L - 1 ? x_out : pp[l & 1]);
+    st = run_mlp(&layers[l], cur, B, t ? t[l] : 0.f, t == nullptr, cur, dst, aux ? &aux[l] : nullptr,
+                 ws, ws_bytes, stream, true, eps);
+    if (st != CATS_OK) return fail(st, "layer %d: %s", l, g_last_error.c_str());
+    cur = dst;
+  }
+  if (x_all) {
+    hipError_t e = hipMemcpyAsync(x_out, cur, rows * sizeof(float), hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "x_out copy");
+  }
+  return CATS_OK;
+}
+
+namespace {
+// Workspace of cats_calibrate_stack: the general region (calibration
+// activations, or the forward's partials while vectors are propagated),
+// then the propagated vectors X and their RMSNorm XN, [N x d] each.
+size_t stack_calib_general(int d, int max_m, int N) {
+  const size_t cal = calib_bytes((int64_t)N * max_m);
+  const size_t fwd = fwd_layout(d, max_m, kMaxBatchTile).end + stack_rows_bytes(d, CATS_MAX_BATCH);
+  return cal > fwd ? cal : fwd;
+}
+}  // namespace
+
+size_t cats_calibrate_stack_workspace_bytes(int32_t d, int32_t max_m, int32_t N) {
+  if (d <= 0 || d % 8 != 0 || d > CATS_MAX_D_BF16 || max_m <= 0 || max_m > CATS_MAX_M || N <= 0 ||
+      N > 4 * 1024 * 1024 || (int64_t)N * max_m > (int64_t)0xffffffffll)
+    return 0;
+  return stack_calib_general(d, max_m, N) + 2 * round_up((size_t)N * d * sizeof(float), kAlign);
+}
+
+cats_status cats_calibrate_stack(const cats_layer* layers, int32_t L, const float* calib_x, int32_t N,
+                                 double sparsity, float eps, void* ws, size_t ws_bytes, void* stream,
+                                 float* t_out) {
+  if (!layers || !calib_x || !t_out) return fail(CATS_ERR_NULL, "layers, calib_x or t_out is NULL");
+  if (L < 1 || L > CATS_MAX_LAYERS) return fail(CATS_ERR_SHAPE, "L=%d outside [1, %d]", (int)L, CATS_MAX_LAYERS);
+  if (N <= 0 || N > 4 * 1024 * 1024) return fail(CATS_ERR_SHAPE, "N=%d out of range", (int)N);
+  if (!aligned(calib_x, 16)) return fail(CATS_ERR_ALIGN, "calib_x must be 16-byte aligned");
+  if (!std::isfinite(sparsity) || sparsity < 0.0 || sparsity > 1.0)
+    return fail(CATS_ERR_RANGE, "sparsity must be in [0, 1]");
+  if (!std::isfinite(eps) || eps < 0.f) return fail(CATS_ERR_RANGE, "eps must be finite and >= 0");
+  const int d = layers[0].d;
+  int max_m = 0;
+  for (int l = 0; l < L; ++l) {
+    cats_status st = check_layer(&layers[l]);
+    if (st != CATS_OK) return fail(st, "layer %d: %s", l, g_last_error.c_str());
+    if (layers[l].d != d) return fail(CATS_ERR_SHAPE, "layer %d has d=%d, layer 0 has d=%d", l, (int)layers[l].d, d);
+    if (layers[l].m > max_m) max_m = layers[l].m;
+  }
+  if ((int64_t)N * max_m > (int64_t)0xffffffffll) return fail(CATS_ERR_SHAPE, "N*m too large");
+  if (sparsity == 0.0) {
+    for (int l = 0; l < L; ++l) t_out[l] = 0.f;
+    return CATS_OK;
+  }
+  const size_t general = stack_calib_general(d, max_m, N);
+  const size_t rows = round_up((size_t)N * d * sizeof(float), kAlign);
+  cats_status st = check_ws(ws, ws_bytes, general + 2 * rows);
+  if (st != CATS_OK) return st;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  float* X = reinterpret_cast<float*>(static_cast<char*>(ws) + general);
+  float* XN = reinterpret_cast<float*>(static_cast<char*>(ws) + general + rows);
+  float* acts = reinterpret_cast<float*>(static_cast<char*>(ws) + radix_bytes());
+  hipError_t e = hipMemcpyAsync(X, calib_x, (size_t)N * d * sizeof(float), hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "calibration vector copy");
+  for (int l = 0; l < L; ++l) {
+    const cats_layer* ly = &layers[l];
+    // what block l sees: the RMSNorm of the densely propagated vectors
+    e = cats::launch_rmsnorm(X, XN, N, d, eps, s);
+    if (e != hipSuccess) return hip_fail(e, "rmsnorm launch");
+    e = cats::launch_calib_acts(ly->wdtype == CATS_BF16, XN, ly->w_gate_t, N, d, ly->m, acts, s);
+    if (e != hipSuccess) return hip_fail(e, "calibration activations launch");
+    st = select_threshold(acts, (int64_t)N * ly->m, sparsity, ws, s, &t_out[l]);
+    if (st != CATS_OK) return st;
+    if (l == L - 1) break;
+    // X <- X + dense MLP_l(XN), CATS_MAX_BATCH rows per call
+    for (int r0 = 0; r0 < N; r0 += CATS_MAX_BATCH) {
+      const int nb = (N - r0) < CATS_MAX_BATCH ? (N - r0) : CATS_MAX_BATCH;
+      float* xr = X + (size_t)r0 * d;
+      st = run_mlp(ly, XN + (size_t)r0 * d, nb, 0.f, true, xr, xr, nullptr, ws, general, stream);
+      if (st != CATS_OK) return fail(st, "layer %d propagation: %s", l, g_last_error.c_str());
+    }
+  }
+  return CATS_OK;
 }
 
 cats_status cats_rmsnorm(const float* x, float* xn, int32_t B, int32_t d, float eps, void* stream) {

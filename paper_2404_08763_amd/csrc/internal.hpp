@@ -36,6 +36,8 @@ struct FusedArgs {
   const float* x;      // [B x d]
   int B, d, m;
   float t;
+  int norm;            // RMSNorm x (unit gain) before the block
+  float eps;           // its epsilon
   float* partial;      // [G x B x d]
   int aux;             // write the union segments for the aux outputs
   int* seg_j;          // [m]

@@ -93,6 +93,13 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
     for (int c = 0; c < NCH; ++c) buf[c] = ld_buf16_stream(r, base + lane_off[c]);
   };
 
+  // Per-row factor on every gate and up dot product: 1, or the RMSNorm
+  // scale 1/sqrt(mean(x^2) + eps) when the block is normalised in front
+  // (x W scaled after the sum equals (x scaled) W up to rounding).
+  float xscale[BT];
+#pragma unroll
+  for (int b = 0; b < BT; ++b) xscale[b] = 1.f;
+
   // Dot products of one weight row with the B staged x rows, wave-summed.
   auto row_dot = [&](const u32x4(&buf)[NCH], float(&out)[BT]) {
     float acc[BT];
@@ -119,7 +126,7 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
       }
     }
 #pragma unroll
-    for (int b = 0; b < BT; ++b) out[b] = (b < B) ? wave_sum(acc[b]) : 0.f;
+    for (int b = 0; b < BT; ++b) out[b] = (b < B) ? wave_sum(acc[b]) * xscale[b] : 0.f;
   };
 
   // ---- stage x (rows past B and columns past d read as zero); its loads
@@ -146,6 +153,28 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
     }
   }
   __syncthreads();
+
+  // ---- optional RMSNorm prologue (unit gain): wave b sums row b's squares
+  // in a fixed order, so every block derives the same scale bit for bit.
+  // It runs while the first gate row is still in flight.
+  if (a.norm) {
+    __shared__ float l_scale[BT];
+    for (int b = w; b < B; b += W) {
+      float ss = 0.f;
+      for (int c = lane * 4; c < DP; c += kWaveSize * 4) {
+        const f32x4 xv = *reinterpret_cast<const f32x4*>(xs + b * DP + c);
+        ss = fmaf(xv.x, xv.x, ss);
+        ss = fmaf(xv.y, xv.y, ss);
+        ss = fmaf(xv.z, xv.z, ss);
+        ss = fmaf(xv.w, xv.w, ss);
+      }
+      ss = wave_sum(ss);
+      if (lane == 0) l_scale[b] = 1.f / sqrtf(ss / (float)d + a.eps);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int b = 0; b < BT; ++b) xscale[b] = (b < B) ? l_scale[b] : 1.f;
+  }
 
   // ---- phase 1: per-wave pipeline over this wave's neurons
   uint32_t pmask = 0;  // row mask of the previous neuron (its up row is in flight)

@@ -1,7 +1,8 @@
 """Seeded synthetic workloads with the shapes of the paper's MLP blocks.
 
 Input generation only: random weights, activations and calibration vectors
-drawn from seeded CPU generators, with no part of the method's arithmetic.
+drawn from seeded generators (CPU; a stack's weights on the device), with no
+part of the method's arithmetic.
 Both the device path and the CPU oracle are fed from these buffers.
 
 The paper times single Llama2-7B (d=4096, m=11008) and Mistral-7B (d=4096,
@@ -9,8 +10,9 @@ m=14336) MLP blocks with real weights and RefinedWeb tokens (Section 5.3);
 neither is available here, so weights are N(0, 0.02^2) and activations are
 synthetic with the distributions below.
 
-Seeds (torch.Generator('cpu').manual_seed):
-  W_gate, W_up, W_down of layer l   1000*l + 0, 1, 2
+Seeds (torch.Generator('cpu').manual_seed unless noted):
+  W_gate, W_up, W_down of layer l   1000*l + 0, 1, 2 (stacks: the device's
+                                    generator, neuron-major; stack_weights)
   calibration vectors               7   (+ 100*l for layer l of a stack)
   decode / test vectors             11
   outlier channel choice            13
@@ -81,6 +83,23 @@ def weights(d: int, m: int, wdtype: torch.dtype, layer: int = 0, std: float = WE
     wu = (torch.randn((d, m), generator=generator(base + 1)) * std).to(wdtype)
     wd = (torch.randn((m, d), generator=generator(base + 2)) * std).to(wdtype)
     return wg, wu, wd
+
+
+def stack_weights(d: int, m: int, wdtype: torch.dtype, layer: int, device="cpu", std: float = WEIGHT_STD):
+    """Neuron-major weights of layer `layer` of a stack: W_gate^T, W_up^T and
+    W_down, each [m, d], drawn in fp32 from N(0, std^2) on `device` (its own
+    Philox generator on a GPU, seeds 1000*layer + 0, 1, 2) and rounded once
+    to `wdtype`.  The entries are iid, so drawing them neuron-major gives the
+    same distribution as drawing the math layout and transposing; a 40-layer
+    stack of 5120 x 13824 blocks is generated in well under a second on a
+    GPU, where the CPU generator would take minutes."""
+    base = 1000 * layer
+    out = []
+    for k in range(3):
+        g = torch.Generator(device=device)
+        g.manual_seed(base + k)
+        out.append((torch.randn((m, d), generator=g, device=device) * std).to(wdtype))
+    return tuple(out)
 
 
 def outlier_channels(d: int, frac: float = 0.01) -> torch.Tensor:

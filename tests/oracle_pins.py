@@ -24,6 +24,11 @@ What pins what:
   calib_acts_vs_library  |SiLU(X W_gate)| against numpy matmul
   calib_analytic         t close to the analytic quantile of |SiLU(sigma Z)|
   rmsnorm_closed_forms   constant rows, the (3,4) row, scale invariance
+  stack_vs_library       x_{l+1} = x_l + MLP_l(RMSNorm(x_l)) over 3 layers
+                         against numpy float64 matmuls, dense and sparse
+                         (per-layer thresholds), with the kept counts
+  stack_infinite_t_is_identity
+                         every neuron masked: each x_l equals x_0 exactly
 """
 from __future__ import annotations
 
@@ -303,6 +308,57 @@ def pin_rmsnorm_closed_forms(O):
     assert np.abs(np.mean(a * a, axis=1) - 1.0).max() <= _tol(O, 1e-6, 1e-12)
 
 
+def _np_stack(x0, layers, ts, eps):
+    """The residual stack through numpy float64 matmuls; the stream is
+    rounded to float32 between layers, as both sides keep it."""
+    x = x0.astype(np.float32)
+    out = [x.copy()]
+    cnts = []
+    for l, (wg, wu, wd) in enumerate(layers):
+        x64 = x.astype(np.float64)
+        xn = (x64 / np.sqrt(np.mean(x64 * x64, axis=1, keepdims=True) + eps)).astype(np.float32)
+        xn = xn.astype(np.float64)
+        v = _np_silu(xn @ wg.astype(np.float64))
+        u = xn @ wu.astype(np.float64)
+        keep = np.ones_like(v, dtype=bool) if ts is None else ~(np.abs(v) < ts[l])
+        cnts.append(keep.sum(axis=1))
+        x = (x64 + (np.where(keep, v * u, 0.0) @ wd.astype(np.float64))).astype(np.float32)
+        out.append(x.copy())
+    return np.stack(out), np.array(cnts)
+
+
+def pin_stack_vs_library(O):
+    r = np.random.default_rng(17)
+    B, d, m, L = 2, 24, 40, 3
+    x0 = (r.standard_normal((B, d)) * 3.0).astype(np.float32)
+    layers = [tuple((r.standard_normal(sh) * 0.3).astype(np.float32) for sh in ((d, m), (d, m), (m, d)))
+              for _ in range(L)]
+    # distinct thresholds per layer, away from every |v| the inputs produce
+    ts = [0.4, 0.9, 0.2]
+    for thr in (None, ts):
+        got, cnt = O.stack(x0, layers, thr, eps=1e-5)
+        exp, ecnt = _np_stack(x0, layers, thr, 1e-5)
+        assert got.shape == (L + 1, B, d)
+        assert np.array_equal(got[0], x0)
+        scale = np.abs(exp).max()
+        assert np.abs(got.astype(np.float64) - exp).max() <= _tol(O, 2e-5, 2e-6) * scale, thr
+        assert np.array_equal(cnt, ecnt), (thr, cnt, ecnt)
+    # the sparse and dense stacks differ (the thresholds drop neurons)
+    assert not np.array_equal(O.stack(x0, layers, ts)[0][-1], O.stack(x0, layers, None)[0][-1])
+
+
+def pin_stack_infinite_t_is_identity(O):
+    r = np.random.default_rng(18)
+    B, d, m, L = 3, 16, 20, 4
+    x0 = r.standard_normal((B, d)).astype(np.float32)
+    layers = [tuple((r.standard_normal(sh) * 0.3).astype(np.float32) for sh in ((d, m), (d, m), (m, d)))
+              for _ in range(L)]
+    got, cnt = O.stack(x0, layers, [math.inf] * L)
+    for l in range(L + 1):
+        assert np.array_equal(got[l], x0)
+    assert not cnt.any()
+
+
 ALL_PINS = [
     pin_silu_closed_forms,
     pin_dense_vs_library,
@@ -317,4 +373,6 @@ ALL_PINS = [
     pin_calib_acts_vs_library,
     pin_calib_analytic,
     pin_rmsnorm_closed_forms,
+    pin_stack_vs_library,
+    pin_stack_infinite_t_is_identity,
 ]

@@ -157,6 +157,79 @@ def test_pack_and_rmsnorm_validation():
     assert L.cats_rmsnorm(ctypes.c_void_p(A), ctypes.c_void_p(A), 1, 8, f(math.nan), None) == RANGE
 
 
+def test_stack_validation():
+    L = P.raw()
+    f = ctypes.c_float
+    lays = (_lib._Layer * 3)(_layer(), _layer(m=200), _layer())
+    ts = (f * 3)(0.1, 0.2, 0.3)
+    need = P.workspace_bytes(64, 200, 2, 0)
+
+    def call(layers=lays, n=3, t=ts, x0=A, B=2, eps=1e-5, out=A + 65536, x_all=None, aux=None,
+             ws=A * 4, ws_bytes=need):
+        return L.cats_stack_forward(layers, n, t, ctypes.c_void_p(x0) if x0 else None, B, f(eps),
+                                    ctypes.c_void_p(out) if out else None,
+                                    ctypes.c_void_p(x_all) if x_all else None, aux,
+                                    ctypes.c_void_p(ws) if ws else None, ws_bytes, None)
+
+    assert call(layers=None) == NULL
+    assert call(x0=0) == NULL
+    assert call(out=0) == NULL
+    assert call(n=0) == SHAPE
+    assert call(n=2000) == SHAPE
+    assert call(B=0) == SHAPE and call(B=17) == SHAPE
+    assert call(eps=-1.0) == RANGE and call(eps=math.nan) == RANGE and call(eps=math.inf) == RANGE
+    assert call(x0=A + 4) == ALIGN and call(x_all=A + 8) == ALIGN
+    assert call(out=A + 64) == RANGE  # x_out overlaps x0
+    bad_t = (f * 3)(0.1, -0.5, 0.3)
+    assert call(t=bad_t) == RANGE
+    assert b"t[1]" in L.cats_last_error()
+    nan_t = (f * 3)(0.1, 0.2, math.nan)
+    assert call(t=nan_t) == RANGE
+    mixed = (_lib._Layer * 3)(_layer(), _layer(d=128), _layer())
+    assert call(layers=mixed) == SHAPE
+    assert b"layer 1" in L.cats_last_error()
+    badw = (_lib._Layer * 3)(_layer(), _layer(), _layer(wg=0))
+    assert call(layers=badw) == NULL and b"layer 2" in L.cats_last_error()
+    aux = (_lib._Aux * 3)()
+    assert call(t=None, aux=aux) == RANGE  # aux outputs need thresholds
+    assert call(ws=0) == WORKSPACE
+    # the workspace must cover the largest layer (m = 200) and the stream rows
+    assert call(ws_bytes=need - 1) == WORKSPACE
+    assert call(ws_bytes=P.workspace_bytes(64, 96, 2, 0)) == WORKSPACE
+
+
+def test_calibrate_stack_validation():
+    L = P.raw()
+    lays = (_lib._Layer * 2)(_layer(), _layer(m=200))
+    t = (ctypes.c_float * 2)(-1.0, -1.0)
+    need = L.cats_calibrate_stack_workspace_bytes(64, 200, 32)
+    assert need > 0
+    assert L.cats_calibrate_stack_workspace_bytes(64, 200, 0) == 0
+    assert L.cats_calibrate_stack_workspace_bytes(12, 200, 8) == 0
+    assert L.cats_calibrate_stack_workspace_bytes(64, 65536, 65536) == 0  # N*m above 2^32
+    assert need > L.cats_calibrate_stack_workspace_bytes(64, 200, 16)
+
+    def call(layers=lays, n=2, x=A, N=32, k=0.5, eps=1e-5, ws=A * 4, ws_bytes=need, tout=t):
+        return L.cats_calibrate_stack(layers, n, ctypes.c_void_p(x) if x else None, N, k, ctypes.c_float(eps),
+                                      ctypes.c_void_p(ws) if ws else None, ws_bytes, None, tout)
+
+    assert call(layers=None) == NULL and call(x=0) == NULL and call(tout=None) == NULL
+    assert call(n=0) == SHAPE and call(N=0) == SHAPE
+    assert call(k=1.5) == RANGE and call(k=math.nan) == RANGE and call(eps=-1.0) == RANGE
+    assert call(x=A + 4) == ALIGN
+    assert call((_lib._Layer * 2)(_layer(), _layer(d=128))) == SHAPE
+    assert call(ws=0) == WORKSPACE and call(ws_bytes=need - 1) == WORKSPACE
+    # k = 0: every threshold is 0, answered on the host
+    assert call(k=0.0) == OK and list(t) == [0.0, 0.0]
+
+
+def test_forward_workspace_is_workspace_bytes():
+    """The forward accepts exactly cats_workspace_bytes(d, m, B, 0) and up."""
+    for B in (1, 3, 8, 16):
+        need = P.workspace_bytes(64, 96, B, 0)
+        assert _fwd(_layer(), B=B, ws_bytes=need - 1) == WORKSPACE
+
+
 def test_timer_interface_without_device():
     L = P.raw()
     assert L.cats_timer_enable(0) == OK

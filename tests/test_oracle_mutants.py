@@ -42,6 +42,12 @@ MUTANTS = {
                      "acts[(size_t)n * m + j] = (double)silu(g[j]);"),
     # RMSNorm over the sum instead of the mean
     "rms_sum": ("ss / (real)d + (real)eps", "ss + (real)eps"),
+    # stack: the MLP fed the raw residual stream instead of its RMSNorm
+    "stack_no_norm": ("rc = oracle_cats_mlp(xn, B, d, m,", "rc = oracle_cats_mlp((float*)xl, B, d, m,"),
+    # stack: the residual connection dropped
+    "stack_no_residual": ("dense ? 0.0 : t[l], dense, xl,", "dense ? 0.0 : t[l], dense, NULL,"),
+    # stack: layer 0's threshold used for every layer
+    "stack_first_t": ("dense ? 0.0 : t[l], dense, xl,", "dense ? 0.0 : t[0], dense, xl,"),
     # v reported before the activation
     "v_before_silu": ("if (v_all) v_all[(size_t)b * m + j] = (double)v;",
                       "if (v_all) v_all[(size_t)b * m + j] = (double)g[j];"),
