@@ -14,7 +14,10 @@ count of that token (full W_gate, plus the active rows of W_up and W_down).
 
 Also reported: per-sparsity us and GB/s, the dense kernel, the roofline of
 the dominant kernel (HIP events on its launch stream over an identical
-timed region), and the CPU oracle on a bounded sample (baseline only).
+timed region), the CPU oracle on a bounded sample (baseline only), and two
+extras: the 40-layer Llama2-13B-shaped stack at k=0.5 (us per layer over a
+128-step decode chain) and the 32-layer Llama2-7B-shaped stack at batch
+1..16 and k=0.5 / 0.7 against dense (where sparsity stops paying).
 """
 from __future__ import annotations
 
@@ -58,6 +61,151 @@ def fused_traffic(cfg_name):
     return int(sum(per) / len(per))
 
 
+def _stack_call(P, stack, x, out, ws, stream):
+    """One raw cats_stack_forward call with prebuilt arguments."""
+    L = P.raw()
+    st = L.cats_stack_forward(stack._arr, len(stack), stack._t, ctypes.c_void_p(x.data_ptr()), x.shape[0],
+                              ctypes.c_float(1e-5), ctypes.c_void_p(out.data_ptr()), None, None,
+                              ctypes.c_void_p(ws.data_ptr()), ws.numel(), stream)
+    if st != 0:
+        raise P.CatsError(st, L.cats_last_error().decode())
+
+
+def _union_counts(P, stack, xb, ws):
+    """|U_l| (the union of the rows' active sets) of every layer, untimed."""
+    import numpy as np
+
+    r = P.stack_forward(stack, xb, ws=ws, aux=True)
+    out = []
+    for a in r["aux"]:
+        cnt = a["cnt"].cpu().numpy()
+        idx = a["idx"].cpu().numpy()
+        out.append(len(np.unique(np.concatenate([idx[b, : cnt[b]] for b in range(len(cnt))]))))
+    return np.array(out)
+
+
+def bench_stack_c4(P, W, torch, timed, steps, warm):
+    """The 40-layer Llama2-13B-shaped stack (d=5120, m=13824, bf16) at
+    k=0.5: thresholds from 1024 calibration vectors propagated densely; a
+    step is one decode vector x_0 ~ N(0,1) through all 40 blocks,
+    x_{l+1} = x_l + MLP_l(RMSNorm(x_l))."""
+    import numpy as np
+
+    c = W.CONFIGS["C4"]
+    dev = torch.device("cuda:0")
+    sw = 2
+    t0 = time.perf_counter()
+    layers = [P.Layer(*W.stack_weights(c.d, c.m, c.wdtype, l, device=dev)) for l in range(c.n_layers)]
+    torch.cuda.synchronize()
+    gen_s = time.perf_counter() - t0
+    xcal = W.calib_vectors(c).to(dev)
+    t0 = time.perf_counter()
+    ts = P.calibrate_stack(P.Stack(layers), xcal, c.sparsities[0])
+    calib_s = time.perf_counter() - t0
+    log(f"[bench] C4 stack: weights {gen_s:.1f} s, calibration {calib_s:.2f} s, t {min(ts):.4f}..{max(ts):.4f}")
+    sparse, dense = P.Stack(layers, ts), P.Stack(layers)
+    xs = W.decode_vectors(c).to(dev)
+    ntok = xs.shape[0]
+    xrows = [xs[i : i + 1] for i in range(ntok)]
+    ws = P.workspace(c.d, c.m, 1, device=dev)
+    out = torch.empty((1, c.d), dtype=torch.float32, device=dev)
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    nact = np.stack([_union_counts(P, sparse, xrows[i], ws) for i in range(ntok)])  # [ntok, L]
+    torch.cuda.synchronize()
+
+    def step_bytes(i):
+        n = nact[i]
+        return int(np.sum(sw * c.d * (c.m + 2 * n) + 8 * c.d + 8 * n))
+
+    ms_s = timed(lambda s: _stack_call(P, sparse, xrows[s % ntok], out, ws, stream), warm, steps)
+    ms_d = timed(lambda s: _stack_call(P, dense, xrows[s % ntok], out, ws, stream), warm, steps)
+    nb = sum(step_bytes((warm + s) % ntok) for s in range(steps))
+    dense_b = steps * c.n_layers * (3 * sw * c.d * c.m + 8 * c.d)
+    Lc = c.n_layers
+    # per-kernel device time inside the stack (events at each kernel's own start and end)
+    P.timer_reset()
+    P.timer_enable(True)
+    timed(lambda s: _stack_call(P, sparse, xrows[s % ntok], out, ws, stream), 0, min(steps, 32))
+    P.timer_enable(False)
+    kt = P.timer_read()
+    n_f, ms_f = kt.get("mlp_fused_cats", (1, 0.0))
+    kb = np.mean([sw * c.d * (c.m + 2 * nact[i % ntok]) + 4 * c.d for i in range(min(steps, 32))])
+    fused_us = ms_f * 1e3 / max(1, n_f)
+    return {
+        "workload": "C4: 40-layer Llama2-13B-shaped MLP stack, d=5120, m=13824, bf16, batch 1, k=0.5",
+        "steps": steps, "layers": Lc,
+        "us_per_layer": round(ms_s * 1e3 / (steps * Lc), 3),
+        "dense_us_per_layer": round(ms_d * 1e3 / (steps * Lc), 3),
+        "stack_ms": round(ms_s / steps, 4), "dense_stack_ms": round(ms_d / steps, 4),
+        "speedup_vs_dense": round(ms_d / ms_s, 3),
+        "gbps": round(nb / (ms_s * 1e-3) / 1e9, 1), "dense_gbps": round(dense_b / (ms_d * 1e-3) / 1e9, 1),
+        "frac_of_hbm_peak": round(nb / (ms_s * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "sparsity_mean": round(float(1 - nact.mean() / c.m), 4),
+        "sparsity_per_layer_min_max": [round(float(1 - nact.mean(0).max() / c.m), 4),
+                                       round(float(1 - nact.mean(0).min() / c.m), 4)],
+        "fused_kernel_avg_us": round(fused_us, 3),
+        "fused_kernel_frac": round(kb / (fused_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+        "kernel_avg_us": {n: round(v[1] * 1e3 / max(1, v[0]), 3) for n, v in kt.items()},
+        "weights_gen_s": round(gen_s, 2), "calib_s": round(calib_s, 2),
+        "thresholds_min_max": [round(min(ts), 5), round(max(ts), 5)],
+    }
+
+
+def bench_batch_c5(P, W, torch, timed, steps, warm):
+    """The 32-layer Llama2-7B-shaped stack at batch 1..16: every row keeps
+    its own mask and each block reads the union of the rows' active W_up /
+    W_down rows once.  Thresholds at k=0.5 and 0.7 from 1024 calibration
+    vectors propagated densely."""
+    import numpy as np
+
+    c = W.CONFIGS["C5"]
+    dev = torch.device("cuda:0")
+    sw = 2
+    layers = [P.Layer(*W.stack_weights(c.d, c.m, c.wdtype, l, device=dev)) for l in range(c.n_layers)]
+    xcal = W.calib_vectors(c).to(dev)
+    ts = {k: P.calibrate_stack(P.Stack(layers), xcal, k) for k in c.sparsities}
+    stacks = {k: P.Stack(layers, ts[k]) for k in c.sparsities}
+    dense = P.Stack(layers)
+    xs = W.decode_vectors(c).to(dev)
+    ntok = xs.shape[0]
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    Lc = c.n_layers
+    res = {"workload": "C5: 32-layer Llama2-7B-shaped MLP stack, d=4096, m=11008, bf16, batch 1..16",
+           "steps": steps, "layers": Lc, "batches": {}}
+    for B in c.batches:
+        nbat = ntok // B
+        xb = [xs[(i * B) % ntok : (i * B) % ntok + B].contiguous() for i in range(nbat)]
+        ws = P.workspace(c.d, c.m, B, device=dev)
+        out = torch.empty((B, c.d), dtype=torch.float32, device=dev)
+        row = {}
+        ms_d = timed(lambda s: _stack_call(P, dense, xb[s % nbat], out, ws, stream), warm, steps)
+        row["dense_us_per_layer"] = round(ms_d * 1e3 / (steps * Lc), 3)
+        # per-kernel device time of the dense stack at this batch
+        P.timer_reset()
+        P.timer_enable(True)
+        timed(lambda s: _stack_call(P, dense, xb[s % nbat], out, ws, stream), 0, 4)
+        P.timer_enable(False)
+        row["dense_kernel_avg_us"] = {n: round(v[1] * 1e3 / max(1, v[0]), 3) for n, v in P.timer_read().items()}
+        for k in c.sparsities:
+            U = np.stack([_union_counts(P, stacks[k], xb[i], ws) for i in range(nbat)])  # [nbat, L]
+            ms = timed(lambda s: _stack_call(P, stacks[k], xb[s % nbat], out, ws, stream), warm, steps)
+            nb = sum(int(np.sum(sw * c.d * (c.m + 2 * U[(warm + s) % nbat]) + 8 * B * c.d)) for s in range(steps))
+            row[str(k)] = {
+                "us_per_layer": round(ms * 1e3 / (steps * Lc), 3),
+                "speedup_vs_dense": round(ms_d / ms, 3),
+                "gbps": round(nb / (ms * 1e-3) / 1e9, 1),
+                "union_frac": round(float(U.mean() / c.m), 4),
+                "bytes_vs_dense": round(float((c.m + 2 * U.mean()) / (3 * c.m)), 4),
+            }
+        res["batches"][str(B)] = row
+        log(f"[bench] C5 B={B}: {row}")
+    for k in c.sparsities:
+        beat = [B for B in c.batches if res["batches"][str(B)][str(k)]["speedup_vs_dense"] > 1.0]
+        res[f"largest_batch_faster_than_dense_k{k}"] = max(beat) if beat else None
+    res["thresholds_k_min_max"] = {str(k): [round(min(v), 5), round(max(v), 5)] for k, v in ts.items()}
+    return res
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -69,6 +217,9 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="only the timed region (for profilers)")
+    ap.add_argument("--no-stacks", action="store_true", help="skip the C4 stack and C5 batch extras")
+    ap.add_argument("--stack-steps", type=int, default=128, help="decode steps of the C4 stack")
+    ap.add_argument("--batch-steps", type=int, default=20, help="steps per batch size of the C5 sweep")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after the timed region, one device-to-device copy of this many MiB "
                          "(a plain copy of known size that scales hardware byte counters)")
@@ -215,6 +366,22 @@ def main() -> int:
         out["dense_gbps"] = round(dense_gbps, 1)
         out["speedup_vs_dense"] = {str(k): round(dense_us / per_k[k][0], 3) for k in ks}
         out["n_act_mean"] = {str(k): round(float(nact[k].mean()), 1) for k in ks}
+        # "Optimal" of the paper's latency comparison: the dense kernel on a
+        # block whose width is the measured mean active count (the first
+        # n rows of each rotated copy), i.e. the same bytes with no masking
+        opt = {}
+        for k in ks:
+            n_opt = max(1, int(round(float(nact[k].mean()))))
+            small = [P.Layer(l.w_gate_t[:n_opt], l.w_up_t[:n_opt], l.w_down[:n_opt]) for l in layers]
+
+            def call_opt(s, small=small):
+                st = dense(small[s % R].c, xptr[s % ntok], 1, None, yptr, wsp, wsn, stream)
+                if st != 0:
+                    raise P.CatsError(st, L.cats_last_error().decode())
+
+            opt[k] = timed(call_opt, Wm, K) * 1e3 / K
+        out["optimal_us_per_layer"] = {str(k): round(opt[k], 3) for k in ks}
+        out["cats_over_optimal"] = {str(k): round(per_k[k][0] / opt[k], 3) for k in ks}
         out["thresholds"] = {str(k): thr[k] for k in ks}
         out["calib_ms"] = round(calib_ms, 2)
 
@@ -238,6 +405,15 @@ def main() -> int:
         }
         out["kernel_avg_us"] = {n: round(v[1] * 1e3 / max(1, v[0]), 3) for n, v in kt.items()}
         out["timed_region_with_kernel_events_ms_per_step"] = round(ms_timer / K, 5)
+
+    if not args.no_extras and not args.no_stacks:
+        del layers, base
+        torch.cuda.empty_cache()
+        out["stack_C4"] = bench_stack_c4(P, W, torch, timed, args.stack_steps, 8)
+        log(f"[bench] C4 stack: {out['stack_C4']}")
+        torch.cuda.empty_cache()
+        out["batch_C5"] = bench_batch_c5(P, W, torch, timed, args.batch_steps, 4)
+        torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
         import oracle

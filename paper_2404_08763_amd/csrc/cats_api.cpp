@@ -48,20 +48,36 @@ struct FwdLayout {
 
 size_t radix_bytes() { return round_up(kRadixWords * sizeof(uint32_t), kAlign); }
 
-FwdLayout fwd_layout(int d, int m, int bp) {
+// Neuron groups and column tiles of the batched down-projection.
+int down_ct(int d) { return (d + cats::kDownCols - 1) / cats::kDownCols; }
+int down_ng(int d, int m) {
   const int G = cats::fused_grid(m);
+  const int ng = cats::kFusedBlocks / down_ct(d);
+  return ng < 1 ? 1 : (ng > G ? G : ng);
+}
+
+// Layout for calls of up to B rows: the partial sums of either path (the
+// fused kernel's per-block partials of one pass of up to kMaxBatchTile rows,
+// or the batched path's per-group partials of all B rows) and the segment
+// lists for B rows.
+FwdLayout fwd_layout(int d, int m, int B) {
+  const int G = cats::fused_grid(m);
+  const int bp = B < kMaxBatchTile ? B : kMaxBatchTile;
+  size_t parts = (size_t)G * bp;
+  const size_t parts_b = (size_t)down_ng(d, m) * B;
+  if (parts_b > parts) parts = parts_b;
   FwdLayout L;
   size_t o = radix_bytes();
   L.partial = o;
-  o = round_up(o + (size_t)G * bp * d * sizeof(float), kAlign);
+  o = round_up(o + parts * d * sizeof(float), kAlign);
   L.seg_j = o;
   o = round_up(o + (size_t)m * sizeof(int32_t), kAlign);
   L.seg_mask = o;
   o = round_up(o + (size_t)m * sizeof(uint32_t), kAlign);
   L.seg_v = o;
-  o = round_up(o + (size_t)bp * m * sizeof(float), kAlign);
+  o = round_up(o + (size_t)B * m * sizeof(float), kAlign);
   L.seg_h = o;
-  o = round_up(o + (size_t)bp * m * sizeof(float), kAlign);
+  o = round_up(o + (size_t)B * m * sizeof(float), kAlign);
   L.seg_cnt = o;
   o = round_up(o + (size_t)cats::kFusedBlocks * sizeof(int32_t), kAlign);
   L.end = o;
@@ -138,7 +154,7 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
   const int nch = cats::fused_nch(bf16, d);
   const int bt_max = cats::fused_bt_max(bf16, nch);
   const int rows_per_pass = B < bt_max ? B : bt_max;
-  const FwdLayout lay = fwd_layout(d, m, rows_per_pass);
+  const FwdLayout lay = fwd_layout(d, m, B);
   // the full cats_workspace_bytes(d, m, B, 0), stack rows included, so one
   // size rule holds for every call
   st = check_ws(ws, ws_bytes, lay.end + stack_rows_bytes(d, B));
@@ -147,6 +163,62 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
   char* w = static_cast<char*>(ws);
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const int G = cats::fused_grid(m);
+  if (bf16 && B >= cats::kBatchedMinRows && cats::batched_ks(d) > 0) {
+    // all rows in one pass: gate/up on the matrix cores, down by column tiles
+    cats::BatchedArgs ba;
+    ba.wg = L->w_gate_t;
+    ba.wu = L->w_up_t;
+    ba.x = x;
+    ba.B = B;
+    ba.d = d;
+    ba.m = m;
+    ba.t = dense ? 0.f : t;
+    ba.norm = norm ? 1 : 0;
+    ba.eps = eps;
+    ba.seg_j = reinterpret_cast<int*>(w + lay.seg_j);
+    ba.seg_mask = reinterpret_cast<uint32_t*>(w + lay.seg_mask);
+    ba.seg_v = reinterpret_cast<float*>(w + lay.seg_v);
+    ba.seg_h = reinterpret_cast<float*>(w + lay.seg_h);
+    ba.seg_cnt = reinterpret_cast<int*>(w + lay.seg_cnt);
+    hipError_t e = cats::launch_gateup(dense, want_aux, ba, G, s);
+    if (e != hipSuccess) return hip_fail(e, "gate/up launch");
+    cats::DownArgs da;
+    da.wd = L->w_down;
+    da.partial = reinterpret_cast<float*>(w + lay.partial);
+    da.seg_j = ba.seg_j;
+    da.seg_h = ba.seg_h;
+    da.seg_cnt = ba.seg_cnt;
+    da.B = B;
+    da.d = d;
+    da.m = m;
+    da.G = G;
+    da.NG = down_ng(d, m);
+    da.CT = down_ct(d);
+    e = cats::launch_down_cols(da, s);
+    if (e != hipSuccess) return hip_fail(e, "down-projection launch");
+    cats::ReduceArgs ra;
+    ra.partial = da.partial;
+    ra.G = da.NG;
+    ra.Gseg = G;
+    ra.B = B;
+    ra.d = d;
+    ra.m = m;
+    ra.residual = residual;
+    ra.y = y;
+    ra.aux = want_aux ? 1 : 0;
+    ra.seg_j = ba.seg_j;
+    ra.seg_mask = ba.seg_mask;
+    ra.seg_v = ba.seg_v;
+    ra.seg_h = ba.seg_h;
+    ra.seg_cnt = ba.seg_cnt;
+    ra.active_idx = want_aux ? aux->active_idx : nullptr;
+    ra.active_cnt = want_aux ? aux->active_cnt : nullptr;
+    ra.active_v = want_aux ? aux->active_v : nullptr;
+    ra.active_h = want_aux ? aux->active_h : nullptr;
+    e = cats::launch_reduce(ra, s);
+    if (e != hipSuccess) return hip_fail(e, "reduce launch");
+    return CATS_OK;
+  }
   for (int b0 = 0; b0 < B; b0 += rows_per_pass) {
     const int bp = (B - b0) < rows_per_pass ? (B - b0) : rows_per_pass;
     cats::FusedArgs fa;
@@ -182,6 +254,7 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
     cats::ReduceArgs ra;
     ra.partial = fa.partial;
     ra.G = G;
+    ra.Gseg = G;
     ra.B = bp;
     ra.d = d;
     ra.m = m;
@@ -356,8 +429,7 @@ size_t cats_workspace_bytes(int32_t d, int32_t m, int32_t max_batch, int64_t max
   if (d <= 0 || d % 8 != 0 || d > CATS_MAX_D_BF16 || m <= 0 || m > CATS_MAX_M || max_batch < 1 ||
       max_batch > CATS_MAX_BATCH || max_calib_values < 0)
     return 0;
-  const int bp = max_batch < kMaxBatchTile ? max_batch : kMaxBatchTile;
-  const size_t fwd = fwd_layout(d, m, bp).end + stack_rows_bytes(d, max_batch);
+  const size_t fwd = fwd_layout(d, m, max_batch).end + stack_rows_bytes(d, max_batch);
   const size_t cal = calib_bytes(max_calib_values);
   return fwd > cal ? fwd : cal;
 }
@@ -463,9 +535,7 @@ cats_status cats_stack_forward(const cats_layer* layers, int32_t L, const float*
     if (st != CATS_OK) return fail(st, "layer %d: %s", l, g_last_error.c_str());
     if (layers[l].d != d) return fail(CATS_ERR_SHAPE, "layer %d has d=%d, layer 0 has d=%d", l, (int)layers[l].d, d);
     if (t && (std::isnan(t[l]) || t[l] < 0.f)) return fail(CATS_ERR_RANGE, "t[%d] must be >= 0 (got %g)", l, (double)t[l]);
-    const int bf16 = layers[l].wdtype == CATS_BF16;
-    const int bt_max = cats::fused_bt_max(bf16, cats::fused_nch(bf16, d));
-    const size_t e = fwd_layout(d, layers[l].m, B < bt_max ? B : bt_max).end;
+    const size_t e = fwd_layout(d, layers[l].m, B).end;
     if (e > fwd_end) fwd_end = e;
   }
   const size_t rows = (size_t)B * d;
@@ -506,7 +576,7 @@ namespace {
 // then the propagated vectors X and their RMSNorm XN, [N x d] each.
 size_t stack_calib_general(int d, int max_m, int N) {
   const size_t cal = calib_bytes((int64_t)N * max_m);
-  const size_t fwd = fwd_layout(d, max_m, kMaxBatchTile).end + stack_rows_bytes(d, CATS_MAX_BATCH);
+  const size_t fwd = fwd_layout(d, max_m, CATS_MAX_BATCH).end + stack_rows_bytes(d, CATS_MAX_BATCH);
   return cal > fwd ? cal : fwd;
 }
 }  // namespace

@@ -17,6 +17,12 @@ namespace cats {
 #ifndef CATS_FUSED_BLOCKS
 #define CATS_FUSED_BLOCKS 256
 #endif
+// Gate rows each wave keeps in flight ahead of the one it reduces (1 or 2).
+#ifndef CATS_GATE_PREFETCH
+#define CATS_GATE_PREFETCH 1
+#endif
+constexpr int kGatePrefetch = CATS_GATE_PREFETCH;
+static_assert(kGatePrefetch == 1 || kGatePrefetch == 2, "gate prefetch depth is 1 or 2");
 constexpr int kFusedWaves = CATS_FUSED_WAVES;
 constexpr int kFusedBlocks = CATS_FUSED_BLOCKS;
 // Neurons a fused-kernel block may own (its LDS lists are this long); with
@@ -47,9 +53,49 @@ struct FusedArgs {
   int* seg_cnt;        // [G]
 };
 
+// Batched path (bf16 weights, kBatchedMinRows..16 rows): gate and up on
+// the matrix cores, then the down-projection by column tiles.  Below 8 rows
+// the fused kernel is faster (one pass of its vector-ALU dot products over
+// the staged rows); above 8 it would need a second pass over the weights.
+#ifndef CATS_BATCHED_MIN_ROWS
+#define CATS_BATCHED_MIN_ROWS 8
+#endif
+constexpr int kBatchedMinRows = CATS_BATCHED_MIN_ROWS;
+constexpr int kBatchedWaves = 8;
+constexpr int kDownCols = kBatchedWaves * 128;  // columns of a down-projection block
+constexpr int kDownRowChunk = 1024;             // rows a down block stages in LDS at once
+
+struct BatchedArgs {
+  const void* wg;      // [m x d] W_gate^T (bf16)
+  const void* wu;      // [m x d] W_up^T
+  const float* x;      // [B x d]
+  int B, d, m;
+  float t;
+  int norm;            // RMSNorm x (unit gain) before the block
+  float eps;           // its epsilon
+  int* seg_j;          // [m] union-active neurons, per block from its first neuron
+  uint32_t* seg_mask;  // [m] their row masks
+  float* seg_v;        // [B x m] (aux only)
+  float* seg_h;        // [B x m]
+  int* seg_cnt;        // [G]
+};
+
+struct DownArgs {
+  const void* wd;      // [m x d] W_down (bf16)
+  float* partial;      // [NG x B x d]
+  const int* seg_j;
+  const float* seg_h;
+  const int* seg_cnt;
+  int B, d, m;
+  int G;               // blocks of the gate/up kernel (segments)
+  int NG;              // neuron groups (partials)
+  int CT;              // column tiles
+};
+
 struct ReduceArgs {
   const float* partial;  // [G x B x d]
   int G, B, d, m;
+  int Gseg;              // segments of the active lists (blocks of the first kernel)
   const float* residual;  // [B x d] or null
   float* y;               // [B x d]
   // aux (finalize) part; all null when not requested
@@ -82,6 +128,12 @@ hipError_t launch_fused_f32_cats(int nch, int bt, const FusedArgs& a, int G, hip
 hipError_t launch_fused_f32_cats_aux(int nch, int bt, const FusedArgs& a, int G, hipStream_t s);
 hipError_t launch_fused_f32_dense(int nch, int bt, const FusedArgs& a, int G, hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
+
+// k-steps of the batched gate/up kernel for width d (0: no instantiation
+// covers d exactly; those widths use the fused kernel).
+int batched_ks(int d);
+hipError_t launch_gateup(bool dense, bool aux, const BatchedArgs& a, int G, hipStream_t s);
+hipError_t launch_down_cols(const DownArgs& a, hipStream_t s);
 
 hipError_t launch_calib_acts(int wdtype_bf16, const float* x, const void* wg_t, int N, int d,
                              int m, float* acts, hipStream_t s);

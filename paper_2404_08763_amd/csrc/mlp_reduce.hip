@@ -8,49 +8,54 @@
 namespace cats {
 
 constexpr int kReduceThreads = 256;
-constexpr int kReduceCols4 = 8;                             // float4 columns per block
-constexpr int kReduceSubs = kReduceThreads / kReduceCols4;  // partial subsets per block
-constexpr int kReducePer = kFusedBlocks / kReduceSubs;      // partials per thread
-static_assert(kFusedBlocks % kReduceSubs == 0, "partials must split evenly over the subsets");
+constexpr int kReduceWaves = kReduceThreads / kWaveSize;    // float4 columns per block
+constexpr int kReducePer = kFusedBlocks / kWaveSize;        // partials per lane
+static_assert(kFusedBlocks % kWaveSize == 0, "partials must split evenly over the lanes");
 
 __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
   const int tid = threadIdx.x;
+  const int lane = tid & (kWaveSize - 1);
   const int d4 = a.d >> 2;
-  const int ncb = (d4 + kReduceCols4 - 1) / kReduceCols4;
+  const int ncb = (d4 + kReduceWaves - 1) / kReduceWaves;
   const int nred = a.B * ncb;
 
   if ((int)blockIdx.x < nred) {
-    // y[b, c] = residual[b, c] + sum over sub (ascending) of (sum over
-    // g = sub + 32 k, ascending k, of partial[g, b, c]); a fixed order, so
-    // deterministic.  All loads of a thread are issued before the first add.
-    __shared__ f32x4 red[kReduceSubs][kReduceCols4];
+    // One wave per float4 column c of row b:
+    //   y[b, c] = residual[b, c] + wave_sum over lanes of
+    //             (sum over k ascending of partial[lane + 64 k, b, c])
+    // a fixed order (the wave sum's tree is fixed), so deterministic.  All
+    // loads, the residual's included, are issued before the first add, and
+    // no LDS or barrier is involved: the kernel costs one memory latency.
     const int b = blockIdx.x / ncb, cb = blockIdx.x - b * ncb;
-    const int cl = tid % kReduceCols4;
-    const int c4 = cb * kReduceCols4 + cl;
-    const int sub = tid / kReduceCols4;
+    const int c4 = __builtin_amdgcn_readfirstlane(cb * kReduceWaves + tid / kWaveSize);
+    if (c4 >= d4) return;  // whole wave
     const __amdgpu_buffer_rsrc_t rp =
         make_rsrc(a.partial, (uint32_t)((size_t)a.G * a.B * a.d * sizeof(float)));
     u32x4 v[kReducePer];
 #pragma unroll
     for (int k = 0; k < kReducePer; ++k) {
-      const int g = sub + k * kReduceSubs;
-      const bool ok = g < a.G && c4 < d4;
-      v[k] = ld_buf16(rp, ok ? (uint32_t)((((size_t)g * a.B + b) * a.d + (size_t)c4 * 4) * sizeof(float)) : kOOB);
+      const int g = lane + k * kWaveSize;
+      v[k] = ld_buf16(rp, g < a.G ? (uint32_t)((((size_t)g * a.B + b) * a.d + (size_t)c4 * 4) * sizeof(float)) : kOOB);
     }
-    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+    u32x4 rv = {0u, 0u, 0u, 0u};
+    if (a.residual) {
+      const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.residual + (size_t)b * a.d, (uint32_t)(a.d * sizeof(float)));
+      rv = ld_buf16(rr, (uint32_t)c4 * 16u);
+    }
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
 #pragma unroll
     for (int k = 0; k < kReducePer; ++k) {
-      f32x4 f = {__uint_as_float(v[k].x), __uint_as_float(v[k].y), __uint_as_float(v[k].z),
-                 __uint_as_float(v[k].w)};
-      s += f;
+      s0 += __uint_as_float(v[k].x);
+      s1 += __uint_as_float(v[k].y);
+      s2 += __uint_as_float(v[k].z);
+      s3 += __uint_as_float(v[k].w);
     }
-    red[sub][cl] = s;
-    __syncthreads();
-    if (sub == 0 && c4 < d4) {
-      f32x4 tot = red[0][cl];
-#pragma unroll
-      for (int k = 1; k < kReduceSubs; ++k) tot += red[k][cl];
-      if (a.residual) tot = reinterpret_cast<const f32x4*>(a.residual + (size_t)b * a.d)[c4] + tot;
+    f32x4 tot = {wave_sum(s0), wave_sum(s1), wave_sum(s2), wave_sum(s3)};
+    if (lane == 0) {
+      if (a.residual) {
+        const f32x4 r = {__uint_as_float(rv.x), __uint_as_float(rv.y), __uint_as_float(rv.z), __uint_as_float(rv.w)};
+        tot = r + tot;
+      }
       reinterpret_cast<f32x4*>(a.y + (size_t)b * a.d)[c4] = tot;
     }
     return;
@@ -62,8 +67,8 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
   // the ascending list.
   __shared__ int offs[kFusedBlocks + 1];
   const int b = blockIdx.x - nred;
-  for (int g = tid; g < a.G; g += kReduceThreads) {
-    const int base = (int)(((int64_t)g * a.m) / a.G);
+  for (int g = tid; g < a.Gseg; g += kReduceThreads) {
+    const int base = (int)(((int64_t)g * a.m) / a.Gseg);
     const int sc = a.seg_cnt[g];
     int mine = 0;
     for (int e = 0; e < sc; ++e) mine += (int)((a.seg_mask[base + e] >> b) & 1u);
@@ -72,16 +77,16 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
   __syncthreads();
   if (tid == 0) {  // exclusive scan over the segment counts
     int run = 0;
-    for (int k = 0; k < a.G; ++k) {
+    for (int k = 0; k < a.Gseg; ++k) {
       const int c = offs[k];
       offs[k] = run;
       run += c;
     }
-    offs[a.G] = run;
+    offs[a.Gseg] = run;
   }
   __syncthreads();
-  for (int g = tid; g < a.G; g += kReduceThreads) {
-    const int base = (int)(((int64_t)g * a.m) / a.G);
+  for (int g = tid; g < a.Gseg; g += kReduceThreads) {
+    const int base = (int)(((int64_t)g * a.m) / a.Gseg);
     const int sc = a.seg_cnt[g];
     int pos = offs[g];
     for (int e = 0; e < sc; ++e) {
@@ -94,12 +99,12 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
       }
     }
   }
-  if (tid == 0 && a.active_cnt) a.active_cnt[b] = offs[a.G];
+  if (tid == 0 && a.active_cnt) a.active_cnt[b] = offs[a.Gseg];
 }
 
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s) {
   const int d4 = a.d >> 2;
-  const int ncb = (d4 + kReduceCols4 - 1) / kReduceCols4;
+  const int ncb = (d4 + kReduceWaves - 1) / kReduceWaves;
   const int grid = a.B * ncb + (a.aux ? a.B : 0);
   KernelTimer timer("k_mlp_reduce", s);
   hipExtLaunchKernelGGL(k_mlp_reduce, dim3(grid), dim3(kReduceThreads), 0, s, timer.start(), timer.stop(), 0,

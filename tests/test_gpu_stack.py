@@ -20,7 +20,7 @@ import torch
 import paper_2404_08763_amd as P
 from paper_2404_08763_amd import workloads as W
 
-from gpu_util import Y_TIGHT, check_forward, device_layer, host_f32, say
+from gpu_util import Y_TIGHT, check_forward, device_layer, h_bound, host_f32, say
 from oracle_pins import _analytic_quantile
 
 pytestmark = pytest.mark.gpu
@@ -47,7 +47,8 @@ def _check_layer(O, layer, hw, x_l, t, B, label):
     xn = _xn(O, x_l)
     ref = O.cats_mlp(xn, *hw, t=t)
     ref_all = O.cats_mlp(xn, *hw, t=0.0)
-    return check_forward(y, r["aux"][0], ref, t, B, label, ref_all=ref_all, w_down=hw[2])
+    return check_forward(y, r["aux"][0], ref, t, B, label, ref_all=ref_all, w_down=hw[2],
+                         h_abs=h_bound(xn, hw[1], ref_all["v"]))
 
 
 # ------------------------------------------------------------ small stacks
@@ -55,14 +56,25 @@ SMALL_D, SMALL_M, SMALL_L = 1032, 693, 4
 SMALL_T = [0.05, 0.12, 0.2, 0.3]
 
 
-@pytest.fixture(scope="module")
-def small(dev):
+def _small_stack(d):
     layers, hws = [], []
     for l in range(SMALL_L):
-        wg, wu, wd = W.weights(SMALL_D, SMALL_M, torch.bfloat16, layer=l)
+        wg, wu, wd = W.weights(d, SMALL_M, torch.bfloat16, layer=l)
         layers.append(device_layer(wg, wu, wd))
         hws.append(host_f32(wg, wu, wd))
     return layers, hws
+
+
+@pytest.fixture(scope="module")
+def small(dev):
+    return _small_stack(SMALL_D)
+
+
+@pytest.fixture(scope="module")
+def small_mfma(dev):
+    """d = 1024: from 8 rows on, bf16 blocks of this width take the
+    matrix-core path, whose RMSNorm is applied inside its gate/up kernel."""
+    return _small_stack(1024)
 
 
 def _x0(B, d, seed=11):
@@ -89,6 +101,23 @@ def test_small_stack_teacher_forced(small, oracle32, B):
     drift = float(np.abs(xa[-1] - xo[-1]).max() / np.abs(xo[-1] - xo[0]).max())
     print(f"[stack] small B={B} active per layer gpu {cnt.mean(axis=1)} oracle {cnto.mean(axis=1)}; "
           f"end-to-end drift {drift:.2e} of ||x_L - x_0||")
+
+
+@pytest.mark.parametrize("B", [8, 16])
+def test_small_stack_teacher_forced_mfma(small_mfma, oracle32, B):
+    layers, hws = small_mfma
+    x0 = _x0(B, 1024, seed=14)
+    xo, cnto = oracle32.stack(x0, hws, SMALL_T, eps=EPS)
+    for l in range(SMALL_L):
+        say("small stack (matrix-core path) B", B, "layer", l, "t", SMALL_T[l])
+        _check_layer(oracle32, layers[l], hws[l], xo[l], SMALL_T[l], B, f"small mfma B{B} l{l}")
+    say("small dense stack chain (matrix-core path) B", B)
+    xd, _ = oracle32.stack(x0, hws, None, eps=EPS)
+    r = P.stack_forward(P.Stack(layers), torch.from_numpy(x0).cuda(), eps=EPS, keep_all=True)
+    xa = r["x_all"].cpu().numpy()
+    for l in range(1, SMALL_L + 1):
+        step = np.abs(xd[l] - xd[l - 1]).max()
+        assert np.abs(xa[l] - xd[l]).max() <= Y_TIGHT * max(step, np.abs(xd[l]).max()), l
 
 
 def test_small_stack_dense_chain(small, oracle32):
@@ -124,12 +153,14 @@ def test_stack_composition_and_identity(small):
     assert torch.equal(inf.view(torch.int32), x0.view(torch.int32))
 
 
-def test_calibrate_stack_small(small, oracle32):
+@pytest.mark.parametrize("which", ["small", "small_mfma"])
+def test_calibrate_stack_small(request, oracle32, which):
     """Per-layer thresholds with dense propagation of the calibration
-    vectors, against the oracle's own propagation and order statistic."""
-    layers, hws = small
+    vectors, against the oracle's own propagation and order statistic (at
+    d = 1024 the propagation's 16-row calls take the matrix-core path)."""
+    layers, hws = request.getfixturevalue(which)
     N = 64
-    xcal = _x0(N, SMALL_D, seed=7)
+    xcal = _x0(N, layers[0].d, seed=7)
     xo, _ = oracle32.stack(xcal, hws, None, eps=EPS)  # dense propagation
     for k in (0.5, 0.9):
         say("calibrate stack k", k)
