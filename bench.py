@@ -199,9 +199,14 @@ def bench_batch_c5(P, W, torch, timed, steps, warm):
             }
         res["batches"][str(B)] = row
         log(f"[bench] C5 B={B}: {row}")
+    # crossover: the smallest batch at which the sparse stack is within 5% of
+    # dense (or slower); predicted: the smallest batch whose union makes the
+    # required bytes at least 95% of dense
     for k in c.sparsities:
-        beat = [B for B in c.batches if res["batches"][str(B)][str(k)]["speedup_vs_dense"] > 1.0]
-        res[f"largest_batch_faster_than_dense_k{k}"] = max(beat) if beat else None
+        meas = [B for B in c.batches if res["batches"][str(B)][str(k)]["speedup_vs_dense"] < 1.05]
+        pred = [B for B in c.batches if res["batches"][str(B)][str(k)]["bytes_vs_dense"] >= 0.95]
+        res[f"crossover_batch_k{k}"] = {"measured": min(meas) if meas else None,
+                                        "from_bytes": min(pred) if pred else None}
     res["thresholds_k_min_max"] = {str(k): [round(min(v), 5), round(max(v), 5)] for k, v in ts.items()}
     return res
 
