@@ -74,6 +74,9 @@ class Oracle:
         L.oracle_cats_mlp.restype = ctypes.c_int
         L.oracle_rmsnorm.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _PD]
         L.oracle_rmsnorm.restype = ctypes.c_int
+        L.oracle_sparse_input_gemv.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _PF,
+                                               ctypes.c_double, _PF, _PD, _PI, _PI]
+        L.oracle_sparse_input_gemv.restype = ctypes.c_int
         _PPF = ctypes.POINTER(_PF)
         L.oracle_stack.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                    _PPF, _PPF, _PPF, _PD, ctypes.c_int32, ctypes.c_double, _PF, _PI]
@@ -136,6 +139,28 @@ class Oracle:
         if self._L.oracle_rmsnorm(_ptr(x, _PF), x.shape[0], x.shape[1], float(eps), _ptr(out, _PD)) != 0:
             raise ValueError("oracle_rmsnorm rejected its arguments")
         return out
+
+    def sparse_input_gemv(self, x, w, t, residual=None):
+        """y = residual + CATS_t(x) W for W [d, n] (see the header).
+
+        Returns a dict with y [B, n], the ascending kept channels of every row
+        and their count."""
+        x = np.ascontiguousarray(x, dtype=_F)
+        if x.ndim == 1:
+            x = x[None, :]
+        B, d = x.shape
+        w = np.ascontiguousarray(w, dtype=_F)
+        assert w.shape[0] == d
+        n = w.shape[1]
+        res = None if residual is None else np.ascontiguousarray(residual, dtype=_F).reshape(B, n)
+        y = np.empty((B, n), _D)
+        idx = np.empty((B, d), np.int32)
+        cnt = np.empty((B,), np.int32)
+        rc = self._L.oracle_sparse_input_gemv(_ptr(x, _PF), B, d, n, _ptr(w, _PF), float(t), _ptr(res, _PF),
+                                              _ptr(y, _PD), _ptr(idx, _PI), _ptr(cnt, _PI))
+        if rc != 0:
+            raise ValueError("oracle_sparse_input_gemv rejected its arguments")
+        return {"y": y, "cnt": cnt.copy(), "idx": [idx[b, : cnt[b]].copy() for b in range(B)]}
 
     def stack(self, x0, layers, ts=None, eps=1e-5):
         """Residual stack x_{l+1} = x_l + MLP_l(RMSNorm(x_l)) (see the header).

@@ -116,6 +116,37 @@ int oracle_rmsnorm(const float* x, int32_t B, int32_t d, double eps, double* out
   return 0;
 }
 
+int oracle_sparse_input_gemv(const float* x, int32_t B, int32_t d, int32_t n, const float* w,
+                             double t_in, const float* residual, double* y, int32_t* active_idx,
+                             int32_t* active_cnt) {
+  if (!x || !w || !y || B <= 0 || d <= 0 || n <= 0) return -1;
+  if (t_in != t_in || t_in < 0) return -1;
+  const real t = (real)t_in;
+  real* s = (real*)malloc(sizeof(real) * (size_t)n);
+  if (!s) return -1;
+  for (int32_t b = 0; b < B; ++b) {
+    const float* xb = x + (size_t)b * d;
+    for (int32_t k = 0; k < n; ++k) s[k] = 0;
+    int32_t cnt = 0;
+    for (int32_t i = 0; i < d; ++i) {
+      const real xc = (real)xb[i];
+      if (!cats_keeps(xc, t)) continue;
+      if (active_idx) active_idx[(size_t)b * d + cnt] = i;
+      ++cnt;
+      const float* w_row = w + (size_t)i * n;
+      for (int32_t k = 0; k < n; ++k) s[k] += xc * (real)w_row[k];
+    }
+    if (active_cnt) active_cnt[b] = cnt;
+    for (int32_t k = 0; k < n; ++k) {
+      real out = s[k];
+      if (residual) out = (real)residual[(size_t)b * n + k] + out;
+      y[(size_t)b * n + k] = (double)out;
+    }
+  }
+  free(s);
+  return 0;
+}
+
 int oracle_stack(const float* x0, int32_t B, int32_t d, int32_t m, int32_t L,
                  const float* const* w_gate, const float* const* w_up,
                  const float* const* w_down, const double* t, int32_t dense, double eps,

@@ -59,6 +59,18 @@ int oracle_cats_mlp(const float* x, int32_t B, int32_t d, int32_t m,
  * the sum of squares taken in ascending i. */
 int oracle_rmsnorm(const float* x, int32_t B, int32_t d, double eps, double* out);
 
+/* CATS on the input of a linear layer (Appendix B wraps the attention
+ * block's input x in CATS_t): y_b = residual_b + CATS_t(x_b) W with
+ * CATS_t(z) = z where |z| >= t, else 0 (Eq. 4).  W is [d x n] row-major, row
+ * i holding input channel i's n output weights.  For every row b the kept
+ * channels are taken in ascending i and s_k = sum_i x_bi W[i, k] accumulates
+ * from +0; y_bk = residual_bk + s_k (residual may be NULL).  Optional:
+ * active_idx[b*d + q] (ascending kept channels), active_cnt[b].  t = 0 keeps
+ * every channel (a plain product).  Returns 0, or -1 on a bad argument. */
+int oracle_sparse_input_gemv(const float* x, int32_t B, int32_t d, int32_t n, const float* w,
+                             double t, const float* residual, double* y, int32_t* active_idx,
+                             int32_t* active_cnt);
+
 /* Residual stack of L gated-MLP blocks, the MLP half of a decoder's layers
  * (norms and residuals sit outside the paper's formulas, Appendix B).  For
  * l = 0 .. L-1 and every row b:

@@ -29,6 +29,9 @@ What pins what:
                          (per-layer thresholds), with the kept counts
   stack_infinite_t_is_identity
                          every neuron masked: each x_l equals x_0 exactly
+  sparse_input_gemv      Appendix B's CATS on a layer input: masked product
+                         vs numpy, t = 0 plain product, t above all |x| is
+                         zero, one kept channel exact, ties kept
 """
 from __future__ import annotations
 
@@ -359,6 +362,36 @@ def pin_stack_infinite_t_is_identity(O):
     assert not cnt.any()
 
 
+def pin_sparse_input_gemv(O):
+    """CATS on a layer's input (Appendix B): against the masked product
+    through numpy float64, t = 0 against the plain product, t above every
+    |x| gives zero (or the residual), one kept channel gives exactly
+    x_i W[i, :], and ties at t are kept."""
+    r = np.random.default_rng(19)
+    B, d, n = 3, 40, 56
+    x = r.standard_normal((B, d)).astype(np.float32)
+    w = (r.standard_normal((d, n)) * 0.3).astype(np.float32)
+    x64, w64 = x.astype(np.float64), w.astype(np.float64)
+    for t in (0.0, 0.6, 1.3):
+        got = O.sparse_input_gemv(x, w, t)
+        keep = ~(np.abs(x64) < t)
+        exp = np.where(keep, x64, 0.0) @ w64
+        assert np.abs(got["y"] - exp).max() <= _tol(O, 2e-6, 1e-12) * max(1.0, np.abs(exp).max()), t
+        for b in range(B):
+            assert np.array_equal(got["idx"][b], np.nonzero(keep[b])[0]), (t, b)
+    big = O.sparse_input_gemv(x, w, float(np.abs(x).max()) * 2)
+    assert not big["y"].any() and not big["cnt"].any()
+    res = r.standard_normal((B, n)).astype(np.float32)
+    assert np.array_equal(O.sparse_input_gemv(x, w, 1e9, residual=res)["y"], res.astype(np.float64))
+    xs = np.zeros((1, d), np.float32)
+    xs[0, 7] = 2.5
+    one = O.sparse_input_gemv(xs, w, 1.0)
+    assert np.array_equal(one["y"][0], (np.float32(2.5) * w[7]).astype(np.float64)) if O.precision == "f32" \
+        else np.array_equal(one["y"][0], 2.5 * w64[7])
+    tie = O.sparse_input_gemv(xs, w, 2.5)
+    assert tie["cnt"][0] == 1
+
+
 ALL_PINS = [
     pin_silu_closed_forms,
     pin_dense_vs_library,
@@ -375,4 +408,5 @@ ALL_PINS = [
     pin_rmsnorm_closed_forms,
     pin_stack_vs_library,
     pin_stack_infinite_t_is_identity,
+    pin_sparse_input_gemv,
 ]

@@ -48,6 +48,11 @@ MUTANTS = {
     "stack_no_residual": ("dense ? 0.0 : t[l], dense, xl,", "dense ? 0.0 : t[l], dense, NULL,"),
     # stack: layer 0's threshold used for every layer
     "stack_first_t": ("dense ? 0.0 : t[l], dense, xl,", "dense ? 0.0 : t[0], dense, xl,"),
+    # input sparsity: strict comparison (ties dropped)
+    "gemv_strict": ("if (!cats_keeps(xc, t)) continue;", "if (!(R_FABS(xc) > t)) continue;"),
+    # input sparsity: W read transposed
+    "gemv_transposed": ("for (int32_t k = 0; k < n; ++k) s[k] += xc * (real)w_row[k];",
+                        "for (int32_t k = 0; k < n; ++k) s[k] += xc * (real)w[((size_t)k * d + i) % ((size_t)d * n)];"),
     # v reported before the activation
     "v_before_silu": ("if (v_all) v_all[(size_t)b * m + j] = (double)v;",
                       "if (v_all) v_all[(size_t)b * m + j] = (double)g[j];"),
