@@ -17,7 +17,8 @@ the dominant kernel (HIP events on its launch stream over an identical
 timed region), the CPU oracle on a bounded sample (baseline only), and two
 extras: the 40-layer Llama2-13B-shaped stack at k=0.5 (us per layer over a
 128-step decode chain) and the 32-layer Llama2-7B-shaped stack at batch
-1..16 and k=0.5 / 0.7 against dense (where sparsity stops paying).
+1..16 and k=0.5 / 0.7 against dense (where sparsity stops paying), and CATS on
+the input of a Mistral-7B-shaped Q/K/V projection (Appendix B).
 """
 from __future__ import annotations
 
@@ -209,6 +210,57 @@ def bench_batch_c5(P, W, torch, timed, steps, warm):
                                         "from_bytes": min(pred) if pred else None}
     res["thresholds_k_min_max"] = {str(k): [round(min(v), 5), round(max(v), 5)] for k, v in ts.items()}
     return res
+
+
+def bench_sparse_input(P, W, torch, timed, steps, warm, rotate):
+    """CATS on the attention input (Appendix B): the Mistral-7B-shaped fused
+    Q/K/V projection (4096 -> 6144, bf16) behind CATS_t at k = 0.5 / 0.7 / 0.9,
+    t from 2048 calibration vectors (Eq. 3 on |x|), one token per call,
+    weight copies rotated as for the MLP; t = 0 is the dense product."""
+    import numpy as np
+
+    c = W.CONFIGS["QKV"]
+    dev = torch.device("cuda:0")
+    d, n = c.d, c.m
+    w0 = W.linear_weight(d, n, c.wdtype, 5000).to(dev)
+    ws_copies = [w0] + [w0.clone() for _ in range(rotate - 1)]
+    xcal = W.calib_vectors(c).to(dev)
+    xs = W.decode_vectors(c).to(dev)
+    ntok = xs.shape[0]
+    thr = {k: P.threshold_from_acts(xcal.reshape(-1).contiguous(), k) for k in c.sparsities}
+    ws = P.sparse_input_workspace(d, n, 1, device=dev)
+    y = torch.empty((1, n), dtype=torch.float32, device=dev)
+    L = P.raw()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    xptr = [ctypes.c_void_p(xs[i : i + 1].data_ptr()) for i in range(ntok)]
+    yptr, wsp, wsn = ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel()
+    wptr = [ctypes.c_void_p(w.data_ptr()) for w in ws_copies]
+
+    def call(s, t):
+        st = L.cats_sparse_input_gemv(wptr[s % rotate], d, n, P.CATS_BF16, xptr[s % ntok], 1, ctypes.c_float(t),
+                                      None, yptr, None, wsp, wsn, stream)
+        if st != 0:
+            raise P.CatsError(st, L.cats_last_error().decode())
+
+    kept = {k: np.array([int((xs[i].abs() >= thr[k]).sum()) for i in range(ntok)]) for k in c.sparsities}
+    out = {"workload": "Mistral-7B-shaped Q/K/V projection 4096 -> 6144 (bf16) behind CATS on its input, batch 1",
+           "steps": steps, "thresholds": {str(k): round(thr[k], 5) for k in c.sparsities}}
+    ms_d = timed(lambda s: call(s, 0.0), warm, steps)
+    out["dense_us"] = round(ms_d * 1e3 / steps, 3)
+    out["dense_gbps"] = round((2 * d * n + 4 * d + 4 * n) / (ms_d * 1e-3 / steps) / 1e9, 1)
+    for k in c.sparsities:
+        ms = timed(lambda s, k=k: call(s, thr[k]), warm, steps)
+        nb = sum(2 * n * int(kept[k][(warm + s) % ntok]) + 4 * d + 4 * n for s in range(steps))
+        out[str(k)] = {"us": round(ms * 1e3 / steps, 3), "gbps": round(nb / (ms * 1e-3) / 1e9, 1),
+                       "frac_of_hbm_peak": round(nb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                       "kept_mean": round(float(kept[k].mean()), 1),
+                       "speedup_vs_dense": round(ms_d / ms, 3)}
+    P.timer_reset()
+    P.timer_enable(True)
+    timed(lambda s: call(s, thr[0.5]), 0, 32)
+    P.timer_enable(False)
+    out["kernel_avg_us_k0.5"] = {nme: round(v[1] * 1e3 / max(1, v[0]), 3) for nme, v in P.timer_read().items() if v[0]}
+    return out
 
 
 def main() -> int:
@@ -418,6 +470,9 @@ def main() -> int:
         log(f"[bench] C4 stack: {out['stack_C4']}")
         torch.cuda.empty_cache()
         out["batch_C5"] = bench_batch_c5(P, W, torch, timed, args.batch_steps, 4)
+        torch.cuda.empty_cache()
+        out["sparse_input_QKV"] = bench_sparse_input(P, W, torch, timed, 200, 20, R)
+        log(f"[bench] sparse-input QKV: {out['sparse_input_QKV']}")
         torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:

@@ -192,6 +192,27 @@ cats_status cats_stack_forward(const cats_layer* layers, int32_t L, const float*
                                float* x_all, const cats_forward_aux* aux, void* ws,
                                size_t ws_bytes, void* stream);
 
+/* CATS on the input of a linear layer.  Appendix B wraps each attention
+ * block's input in CATS_t, so its query / key / value projections take a
+ * sparse input:
+ *   y_b = residual_b + CATS_t(x_b) W,   CATS_t(z) = z where |z| >= t, else 0
+ * (Eq. 4, ties kept).  Only the rows of W of the channels some batch row
+ * keeps are read (the union over rows; each row keeps its own channels).
+ *   w        dev [d x n] row-major, row i = input channel i (bf16 only:
+ *            CATS_F32 returns CATS_ERR_UNIMPLEMENTED); 1 <= d <= CATS_MAX_M,
+ *            n a positive multiple of 8, d * n * 2 <= CATS_MAX_MATRIX_BYTES
+ *   x        dev [B x d] fp32, 1 <= B <= CATS_MAX_BATCH
+ *   residual dev [B x n] or NULL;  y dev [B x n] (must not alias x)
+ *   aux      per row, ascending: active_idx [B x d] kept channels,
+ *            active_cnt [B], active_v = active_h [B x d] their values; or NULL
+ * t >= 0; t = 0 keeps every channel (the dense product).  Workspace:
+ * cats_sparse_input_workspace_bytes(d, n, B).  Enqueue only. */
+size_t cats_sparse_input_workspace_bytes(int32_t d, int32_t n, int32_t max_batch);
+cats_status cats_sparse_input_gemv(const void* w, int32_t d, int32_t n, int32_t wdtype,
+                                   const float* x, int32_t B, float t, const float* residual,
+                                   float* y, const cats_forward_aux* aux, void* ws,
+                                   size_t ws_bytes, void* stream);
+
 /* Per-block cutoffs of a stack (Eq. 3 for every block, Section 4.1): the
  * N calibration vectors (dev [N x d] fp32, the residual stream entering
  * layer 0) are propagated through the stack densely, as the thresholds

@@ -23,6 +23,8 @@ from ._lib import (  # noqa: F401
     Stack,
     calibrate_stack,
     rmsnorm,
+    sparse_input_gemv,
+    sparse_input_workspace,
     stack_forward,
     threshold_from_acts,
     timer_enable,

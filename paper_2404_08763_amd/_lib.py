@@ -70,6 +70,9 @@ _SIGNATURES = {
     "cats_calibrate_stack_workspace_bytes": ([_i32, _i32, _i32], _sz),
     "cats_calibrate_stack": ([ctypes.POINTER(_Layer), _i32, _vp, _i32, _f64, _f32, _vp, _sz, _vp,
                               ctypes.POINTER(_f32)], _i32),
+    "cats_sparse_input_workspace_bytes": ([_i32, _i32, _i32], _sz),
+    "cats_sparse_input_gemv": ([_vp, _i32, _i32, _i32, _vp, _i32, _f32, _vp, _vp, ctypes.POINTER(_Aux), _vp,
+                                _sz, _vp], _i32),
     "cats_rmsnorm": ([_vp, _vp, _i32, _i32, _f32, _vp], _i32),
     "cats_timer_enable": ([_i32], _i32),
     "cats_timer_reset": ([], _i32),
@@ -360,6 +363,48 @@ def calibrate_stack(stack: Stack, calib_x: torch.Tensor, sparsity: float, eps: f
     _check(raw().cats_calibrate_stack(stack._arr, L, _ptr(calib_x), N, float(sparsity), float(eps),
                                       _ptr(ws), ws.numel(), _stream(), t))
     return [float(v) for v in t]
+
+
+def sparse_input_workspace(d: int, n: int, max_batch: int = 1, device="cuda") -> torch.Tensor:
+    nbytes = int(raw().cats_sparse_input_workspace_bytes(d, n, max_batch))
+    if nbytes == 0:
+        raise ValueError("arguments outside the supported range")
+    return torch.zeros(nbytes, dtype=torch.uint8, device=device)
+
+
+def sparse_input_gemv(w: torch.Tensor, x: torch.Tensor, t: float, residual: Optional[torch.Tensor] = None,
+                      out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, aux: bool = False):
+    """y = residual + CATS_t(x) W for W [d, n] (channel-major, bf16).
+
+    Returns y, or (y, aux dict) with per row the ascending kept channels
+    idx[b, :cnt[b]] and their values v (= h)."""
+    _dev(w, "w", torch.bfloat16)
+    _dev(x, "x", torch.float32)
+    d, n = int(w.shape[0]), int(w.shape[1])
+    B = _rows(x)
+    if out is None:
+        out = torch.empty((B, n), dtype=torch.float32, device=x.device)
+    _dev(out, "out", torch.float32)
+    if residual is not None:
+        _dev(residual, "residual", torch.float32)
+    if ws is None:
+        ws = sparse_input_workspace(d, n, B, device=x.device)
+    aux_c = None
+    bufs = None
+    if aux:
+        bufs = {
+            "idx": torch.empty((B, d), dtype=torch.int32, device=x.device),
+            "cnt": torch.empty((B,), dtype=torch.int32, device=x.device),
+            "v": torch.empty((B, d), dtype=torch.float32, device=x.device),
+            "h": torch.empty((B, d), dtype=torch.float32, device=x.device),
+        }
+        aux_c = _Aux(bufs["idx"].data_ptr(), bufs["cnt"].data_ptr(), bufs["v"].data_ptr(), bufs["h"].data_ptr())
+    _check(raw().cats_sparse_input_gemv(_ptr(w), d, n, CATS_BF16, _ptr(x), B, float(t), _ptr(residual),
+                                        _ptr(out), ctypes.byref(aux_c) if aux_c is not None else None,
+                                        _ptr(ws), ws.numel(), _stream()))
+    if aux:
+        return out, bufs
+    return out
 
 
 def rmsnorm(x: torch.Tensor, eps: float = 1e-5, out: Optional[torch.Tensor] = None) -> torch.Tensor:

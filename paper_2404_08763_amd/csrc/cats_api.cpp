@@ -2,6 +2,7 @@
 // call), workspace carving, kernel dispatch and the optional kernel timer.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -200,6 +201,7 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
     ra.partial = da.partial;
     ra.G = da.NG;
     ra.Gseg = G;
+    ra.sum_y = 1;
     ra.B = B;
     ra.d = d;
     ra.m = m;
@@ -255,6 +257,7 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
     ra.partial = fa.partial;
     ra.G = G;
     ra.Gseg = G;
+    ra.sum_y = 1;
     ra.B = bp;
     ra.d = d;
     ra.m = m;
@@ -566,6 +569,138 @@ cats_status cats_stack_forward(const cats_layer* layers, int32_t L, const float*
   if (x_all) {
     hipError_t e = hipMemcpyAsync(x_out, cur, rows * sizeof(float), hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return hip_fail(e, "x_out copy");
+  }
+  return CATS_OK;
+}
+
+namespace {
+// Workspace of cats_sparse_input_gemv: the groups' partial sums, the
+// column tiles' tickets and the segment lists over the d input channels.
+struct GemvLayout {
+  size_t partial, tickets, seg_j, seg_mask, seg_v, seg_h, seg_cnt, end;
+  int NG, CT;
+};
+
+GemvLayout gemv_layout(int d, int n, int B) {
+  GemvLayout L;
+  L.CT = (n + cats::kSparseCols - 1) / cats::kSparseCols;
+  // about one block per compute unit; one group once the column tiles alone
+  // fill most of the chip
+  L.NG = (cats::kFusedBlocks + L.CT / 2) / L.CT;
+  if (L.NG < 1) L.NG = 1;
+  if (L.NG > d) L.NG = d;
+  if (L.NG > cats::kFusedBlocks) L.NG = cats::kFusedBlocks;
+  size_t o = radix_bytes();
+  L.partial = o;
+  o = round_up(o + (size_t)L.NG * B * n * sizeof(float), kAlign);
+  L.tickets = o;
+  o = round_up(o + (size_t)L.CT * sizeof(unsigned long long), kAlign);
+  L.seg_j = o;
+  o = round_up(o + (size_t)d * sizeof(int32_t), kAlign);
+  L.seg_mask = o;
+  o = round_up(o + (size_t)d * sizeof(uint32_t), kAlign);
+  L.seg_v = o;
+  o = round_up(o + (size_t)B * d * sizeof(float), kAlign);
+  L.seg_h = o;
+  o = round_up(o + (size_t)B * d * sizeof(float), kAlign);
+  L.seg_cnt = o;
+  o = round_up(o + (size_t)cats::kFusedBlocks * sizeof(int32_t), kAlign);
+  L.end = o;
+  return L;
+}
+
+// Tags of successive sparse-input calls (never 0), so a column tile's
+// ticket word left by any earlier call is recognised as stale.
+std::atomic<uint32_t> g_epoch{0};
+uint32_t next_epoch() {
+  uint32_t e;
+  do {
+    e = g_epoch.fetch_add(1u, std::memory_order_relaxed) + 1u;
+  } while (e == 0u);
+  return e;
+}
+
+bool gemv_shape_ok(int d, int n) {
+  return d > 0 && d <= CATS_MAX_M && n > 0 && n % 8 == 0 && (uint64_t)d * n * 2 <= CATS_MAX_MATRIX_BYTES;
+}
+}  // namespace
+
+size_t cats_sparse_input_workspace_bytes(int32_t d, int32_t n, int32_t max_batch) {
+  if (!gemv_shape_ok(d, n) || max_batch < 1 || max_batch > CATS_MAX_BATCH) return 0;
+  return gemv_layout(d, n, max_batch).end;
+}
+
+cats_status cats_sparse_input_gemv(const void* w, int32_t d, int32_t n, int32_t wdtype, const float* x,
+                                   int32_t B, float t, const float* residual, float* y,
+                                   const cats_forward_aux* aux, void* ws, size_t ws_bytes, void* stream) {
+  if (!w || !x || !y) return fail(CATS_ERR_NULL, "w, x or y is NULL");
+  if (wdtype != CATS_BF16 && wdtype != CATS_F32) return fail(CATS_ERR_DTYPE, "unknown weight dtype %d", (int)wdtype);
+  if (wdtype != CATS_BF16) return fail(CATS_ERR_UNIMPLEMENTED, "the sparse-input product takes bf16 weights");
+  if (!gemv_shape_ok(d, n))
+    return fail(CATS_ERR_SHAPE, "d=%d must be in [1, %d], n=%d a positive multiple of 8, d*n*2 at most %llu bytes",
+                (int)d, CATS_MAX_M, (int)n, (unsigned long long)CATS_MAX_MATRIX_BYTES);
+  if (B < 1 || B > CATS_MAX_BATCH) return fail(CATS_ERR_SHAPE, "B=%d outside [1, %d]", (int)B, CATS_MAX_BATCH);
+  if (!aligned(w, 16) || !aligned(x, 4) || !aligned(y, 16) || (residual && !aligned(residual, 16)))
+    return fail(CATS_ERR_ALIGN, "w, y and residual must be 16-byte aligned, x 4-byte aligned");
+  if (std::isnan(t) || t < 0.f) return fail(CATS_ERR_RANGE, "t must be >= 0 (got %g)", (double)t);
+  const bool want_aux = aux && (aux->active_idx || aux->active_cnt || aux->active_v || aux->active_h);
+  if (want_aux && ((aux->active_idx && !aligned(aux->active_idx, 4)) ||
+                   (aux->active_cnt && !aligned(aux->active_cnt, 4)) ||
+                   (aux->active_v && !aligned(aux->active_v, 4)) ||
+                   (aux->active_h && !aligned(aux->active_h, 4))))
+    return fail(CATS_ERR_ALIGN, "aux outputs must be 4-byte aligned");
+  const GemvLayout lay = gemv_layout(d, n, B);
+  cats_status st = check_ws(ws, ws_bytes, lay.end);
+  if (st != CATS_OK) return st;
+  char* wsp = static_cast<char*>(ws);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+
+  cats::SparseInputArgs sa;
+  sa.w = w;
+  sa.x = x;
+  sa.residual = residual;
+  sa.y = y;
+  sa.B = B;
+  sa.d = d;
+  sa.n = n;
+  sa.t = t;
+  sa.NG = lay.NG;
+  sa.CT = lay.CT;
+  sa.partial = reinterpret_cast<float*>(wsp + lay.partial);
+  sa.tickets = reinterpret_cast<unsigned long long*>(wsp + lay.tickets);
+  sa.epoch = next_epoch();
+  sa.aux = want_aux ? 1 : 0;
+  sa.seg_j = reinterpret_cast<int*>(wsp + lay.seg_j);
+  sa.seg_mask = reinterpret_cast<uint32_t*>(wsp + lay.seg_mask);
+  sa.seg_v = reinterpret_cast<float*>(wsp + lay.seg_v);
+  sa.seg_h = reinterpret_cast<float*>(wsp + lay.seg_h);
+  sa.seg_cnt = reinterpret_cast<int*>(wsp + lay.seg_cnt);
+  hipError_t e = cats::launch_sparse_input(sa, s);
+  if (e != hipSuccess) return hip_fail(e, "sparse-input product launch");
+  if (want_aux) {
+    // the per-row active lists from the groups' segments (y is written)
+    cats::ReduceArgs ra;
+    ra.partial = nullptr;
+    ra.G = lay.NG;
+    ra.Gseg = lay.NG;
+    ra.sum_y = 0;
+    ra.B = B;
+    ra.d = n;
+    ra.m = d;
+    ra.residual = nullptr;
+    ra.y = nullptr;
+    ra.aux = 1;
+    ra.seg_j = sa.seg_j;
+    ra.seg_mask = sa.seg_mask;
+    ra.seg_v = sa.seg_v;
+    ra.seg_h = sa.seg_h;
+    ra.seg_cnt = sa.seg_cnt;
+    ra.active_idx = aux->active_idx;
+    ra.active_cnt = aux->active_cnt;
+    ra.active_v = aux->active_v;
+    ra.active_h = aux->active_h;
+    e = cats::launch_reduce(ra, s);
+    if (e != hipSuccess) return hip_fail(e, "active-list launch");
   }
   return CATS_OK;
 }

@@ -53,6 +53,19 @@ __device__ __forceinline__ u32x4 ld_buf16(__amdgpu_buffer_rsrc_t r, uint32_t off
   return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
 }
 
+// Device-coherent 16-byte load and store (cache policy sc1): they reach the
+// memory level shared by every XCD, so blocks on different XCDs can exchange
+// data within one kernel without a cache-wide write-back or invalidation.
+constexpr int kCachePolicySc1 = 16;
+
+__device__ __forceinline__ u32x4 ld_buf16_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kCachePolicySc1);
+}
+
+__device__ __forceinline__ void st_buf16_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off, u32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)off, 0, kCachePolicySc1);
+}
+
 __device__ __forceinline__ u32x4 zero_u32x4() {
   u32x4 z = {0u, 0u, 0u, 0u};
   return z;

@@ -92,10 +92,37 @@ struct DownArgs {
   int CT;              // column tiles
 };
 
+// Rows of one call (the C ABI's CATS_MAX_BATCH).
+constexpr int kMaxRows = 16;
+
+// CATS on a layer's input (k_sparse_input): output columns per block (a
+// 256-byte slice of each weight row; 32 and 64 are also valid).
+constexpr int kSparseCols = 128;
+
+struct SparseInputArgs {
+  const void* w;            // [d x n] bf16, row i = input channel i
+  const float* x;           // [B x d]
+  const float* residual;    // [B x n] or null
+  float* y;                 // [B x n]
+  int B, d, n;
+  float t;
+  int NG, CT;               // input-channel groups, column tiles
+  float* partial;           // [NG x B x n] (NG > 1)
+  unsigned long long* tickets;  // [CT] epoch-tagged arrival counts
+  uint32_t epoch;           // this call's tag (never 0)
+  int aux;                  // blocks of column tile 0 write the segments
+  int* seg_j;               // [d] kept channels, per group from its first channel
+  uint32_t* seg_mask;       // [d]
+  float* seg_v;             // [B x d]
+  float* seg_h;             // [B x d]
+  int* seg_cnt;             // [NG]
+};
+
 struct ReduceArgs {
   const float* partial;  // [G x B x d]
   int G, B, d, m;
   int Gseg;              // segments of the active lists (blocks of the first kernel)
+  int sum_y;             // 0: only the active lists (y is already written)
   const float* residual;  // [B x d] or null
   float* y;               // [B x d]
   // aux (finalize) part; all null when not requested
@@ -134,6 +161,7 @@ hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 int batched_ks(int d);
 hipError_t launch_gateup(bool dense, bool aux, const BatchedArgs& a, int G, hipStream_t s);
 hipError_t launch_down_cols(const DownArgs& a, hipStream_t s);
+hipError_t launch_sparse_input(const SparseInputArgs& a, hipStream_t s);
 
 hipError_t launch_calib_acts(int wdtype_bf16, const float* x, const void* wg_t, int N, int d,
                              int m, float* acts, hipStream_t s);

@@ -17,7 +17,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
   const int lane = tid & (kWaveSize - 1);
   const int d4 = a.d >> 2;
   const int ncb = (d4 + kReduceWaves - 1) / kReduceWaves;
-  const int nred = a.B * ncb;
+  const int nred = a.sum_y ? a.B * ncb : 0;
 
   if ((int)blockIdx.x < nred) {
     // One wave per float4 column c of row b:
@@ -105,7 +105,8 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s) {
   const int d4 = a.d >> 2;
   const int ncb = (d4 + kReduceWaves - 1) / kReduceWaves;
-  const int grid = a.B * ncb + (a.aux ? a.B : 0);
+  const int grid = (a.sum_y ? a.B * ncb : 0) + (a.aux ? a.B : 0);
+  if (grid == 0) return hipSuccess;
   KernelTimer timer("k_mlp_reduce", s);
   hipExtLaunchKernelGGL(k_mlp_reduce, dim3(grid), dim3(kReduceThreads), 0, s, timer.start(), timer.stop(), 0,
                         a);

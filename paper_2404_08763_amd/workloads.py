@@ -17,6 +17,7 @@ Seeds (torch.Generator('cpu').manual_seed unless noted):
   decode / test vectors             11
   outlier channel choice            13
   mixture scales                    17
+  Q/K/V projection weight           5000
 """
 from __future__ import annotations
 
@@ -61,6 +62,10 @@ CONFIGS = {
                  notes="Mistral-7B-shaped MLP, Laplace(0,1) scale mixture"),
     "C4": Config("C4", d=5120, m=13824, wdtype=torch.bfloat16, n_calib=1024, n_decode=128,
                  sparsities=(0.5,), n_layers=40, notes="Llama2-13B-shaped 40-layer stack"),
+    "QKV": Config("QKV", d=4096, m=6144, wdtype=torch.bfloat16, n_calib=2048, n_decode=256,
+                  sparsities=(0.5, 0.7, 0.9), x_dist="laplace_mix",
+                  notes="Mistral-7B-shaped fused Q/K/V projection (4096 -> 4096 + 1024 + 1024) "
+                        "behind CATS on its input; m is the output width n"),
     "C5": Config("C5", d=4096, m=11008, wdtype=torch.bfloat16, n_calib=1024, n_decode=64,
                  sparsities=(0.5, 0.7), n_layers=32, batches=(1, 2, 4, 8, 16),
                  notes="Llama2-7B-shaped 32-layer stack, small-batch decode"),
@@ -100,6 +105,12 @@ def stack_weights(d: int, m: int, wdtype: torch.dtype, layer: int, device="cpu",
         g.manual_seed(base + k)
         out.append((torch.randn((m, d), generator=g, device=device) * std).to(wdtype))
     return tuple(out)
+
+
+def linear_weight(d: int, n: int, wdtype: torch.dtype, seed: int, std: float = WEIGHT_STD) -> torch.Tensor:
+    """A linear layer's weight in channel-major layout [d, n] (row i = input
+    channel i), N(0, std^2) drawn in fp32 (CPU generator) and rounded once."""
+    return (torch.randn((d, n), generator=generator(seed)) * std).to(wdtype)
 
 
 def outlier_channels(d: int, frac: float = 0.01) -> torch.Tensor:

@@ -223,6 +223,33 @@ def test_calibrate_stack_validation():
     assert call(k=0.0) == OK and list(t) == [0.0, 0.0]
 
 
+def test_sparse_input_validation():
+    L = P.raw()
+    f = ctypes.c_float
+    need = L.cats_sparse_input_workspace_bytes(64, 96, 2)
+    assert need > 0
+    assert L.cats_sparse_input_workspace_bytes(64, 100, 1) == 0  # n not a multiple of 8
+    assert L.cats_sparse_input_workspace_bytes(0, 96, 1) == 0
+    assert L.cats_sparse_input_workspace_bytes(64, 96, 17) == 0
+    assert L.cats_sparse_input_workspace_bytes(65536, 1 << 14, 1) == 0  # 2 GiB of weights
+
+    def call(w=A, d=64, n=96, dt=P.CATS_BF16, x=A + 65536, B=2, t=0.5, res=None, y=A * 2, ws=A * 4,
+             ws_bytes=need):
+        return L.cats_sparse_input_gemv(ctypes.c_void_p(w) if w else None, d, n, dt,
+                                        ctypes.c_void_p(x) if x else None, B, f(t),
+                                        ctypes.c_void_p(res) if res else None, ctypes.c_void_p(y) if y else None,
+                                        None, ctypes.c_void_p(ws) if ws else None, ws_bytes, None)
+
+    assert call(w=0) == NULL and call(x=0) == NULL and call(y=0) == NULL
+    assert call(dt=7) == DTYPE
+    assert call(dt=P.CATS_F32) == 8  # CATS_ERR_UNIMPLEMENTED
+    assert call(n=100) == SHAPE and call(d=0) == SHAPE and call(B=0) == SHAPE and call(B=17) == SHAPE
+    assert call(w=A + 8) == ALIGN and call(x=A + 2) == ALIGN and call(y=A + 4) == ALIGN
+    assert call(res=A + 4) == ALIGN
+    assert call(t=-1.0) == RANGE and call(t=math.nan) == RANGE
+    assert call(ws=0) == WORKSPACE and call(ws_bytes=need - 1) == WORKSPACE
+
+
 def test_forward_workspace_is_workspace_bytes():
     """The forward accepts exactly cats_workspace_bytes(d, m, B, 0) and up."""
     for B in (1, 3, 8, 16):
