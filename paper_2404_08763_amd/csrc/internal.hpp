@@ -17,12 +17,6 @@ namespace cats {
 #ifndef CATS_FUSED_BLOCKS
 #define CATS_FUSED_BLOCKS 256
 #endif
-// Gate rows each wave keeps in flight ahead of the one it reduces (1 or 2).
-#ifndef CATS_GATE_PREFETCH
-#define CATS_GATE_PREFETCH 1
-#endif
-constexpr int kGatePrefetch = CATS_GATE_PREFETCH;
-static_assert(kGatePrefetch == 1 || kGatePrefetch == 2, "gate prefetch depth is 1 or 2");
 constexpr int kFusedWaves = CATS_FUSED_WAVES;
 constexpr int kFusedBlocks = CATS_FUSED_BLOCKS;
 // Neurons a fused-kernel block may own (its LDS lists are this long); with

@@ -132,7 +132,7 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
   // ---- stage x (rows past B and columns past d read as zero); its loads
   // go out first so the first gate row can stay in flight while x is
   // written to LDS
-  u32x4 gA[NCH], gB[NCH], gC[NCH], uA[NCH], uB[NCH];
+  u32x4 gA[NCH], gB[NCH], uA[NCH], uB[NCH];
   {
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, (uint32_t)(B * d * sizeof(float)));
     constexpr int NV = BT * DP / 4;  // float4 slots in LDS
@@ -146,7 +146,6 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
       xv[k] = ld_buf16(rx, ok ? (uint32_t)((b * d + c) * sizeof(float)) : kOOB);
     }
     load_row(gA, rg, row_base(0 < ni, n0 + w));
-    if constexpr (kGatePrefetch == 2) load_row(gB, rg, row_base(1 < ni, n0 + w + W));
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int i4 = tid + k * NT;
@@ -183,11 +182,11 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
 #pragma unroll
   for (int b = 0; b < BT; ++b) pv[b] = 0.f;
 
-  // iteration i: prefetch gate(i+P) into gnxt; gate(i) -> mask, issue
-  // up(i); finish up(i-1).  P = kGatePrefetch gate rows stay in flight.
+  // iteration i: prefetch gate(i+1) into gnxt; gate(i) -> mask, issue
+  // up(i); finish up(i-1).
   auto iter = [&](int i, u32x4(&gcur)[NCH], u32x4(&gnxt)[NCH], u32x4(&ucur)[NCH],
                   u32x4(&uprev)[NCH]) {
-    load_row(gnxt, rg, row_base(i + kGatePrefetch < ni, n0 + w + (i + kGatePrefetch) * W));
+    load_row(gnxt, rg, row_base(i + 1 < ni, n0 + w + (i + 1) * W));
     uint32_t mask = 0;
     float v[BT];
 #pragma unroll
@@ -229,21 +228,9 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
   };
   // Two neurons per trip so buffers alternate without copies (a copy would
   // wait for the load it copies).
-  if constexpr (kGatePrefetch == 1) {
-    for (int i = 0; i <= ni; i += 2) {
-      iter(i, gA, gB, uA, uB);
-      if (i + 1 <= ni) iter(i + 1, gB, gA, uB, uA);
-    }
-  } else {
-    // three gate buffers and two up buffers: six neurons per trip
-    for (int i = 0; i <= ni; i += 6) {
-      iter(i, gA, gC, uA, uB);
-      if (i + 1 <= ni) iter(i + 1, gB, gA, uB, uA);
-      if (i + 2 <= ni) iter(i + 2, gC, gB, uA, uB);
-      if (i + 3 <= ni) iter(i + 3, gA, gC, uB, uA);
-      if (i + 4 <= ni) iter(i + 4, gB, gA, uA, uB);
-      if (i + 5 <= ni) iter(i + 5, gC, gB, uB, uA);
-    }
+  for (int i = 0; i <= ni; i += 2) {
+    iter(i, gA, gB, uA, uB);
+    if (i + 1 <= ni) iter(i + 1, gB, gA, uB, uA);
   }
   __syncthreads();
 
