@@ -77,6 +77,9 @@ class Oracle:
         L.oracle_sparse_input_gemv.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _PF,
                                                ctypes.c_double, _PF, _PD, _PI, _PI]
         L.oracle_sparse_input_gemv.restype = ctypes.c_int
+        L.oracle_topk_thresholds.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _PF,
+                                             ctypes.c_double, _PD]
+        L.oracle_topk_thresholds.restype = ctypes.c_int
         _PPF = ctypes.POINTER(_PF)
         L.oracle_stack.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                    _PPF, _PPF, _PPF, _PD, ctypes.c_int32, ctypes.c_double, _PF, _PI]
@@ -138,6 +141,36 @@ class Oracle:
         out = np.empty(x.shape, _D)
         if self._L.oracle_rmsnorm(_ptr(x, _PF), x.shape[0], x.shape[1], float(eps), _ptr(out, _PD)) != 0:
             raise ValueError("oracle_rmsnorm rejected its arguments")
+        return out
+
+    def topk_thresholds(self, x, w_gate, k):
+        """Per-row cutoffs of the top-k variant (see the header): t [B]."""
+        x = np.ascontiguousarray(x, dtype=_F)
+        if x.ndim == 1:
+            x = x[None, :]
+        B, d = x.shape
+        w_gate = np.ascontiguousarray(w_gate, dtype=_F)
+        m = w_gate.shape[1]
+        t = np.empty((B,), _D)
+        if self._L.oracle_topk_thresholds(_ptr(x, _PF), B, d, m, _ptr(w_gate, _PF), float(k), _ptr(t, _PD)) != 0:
+            raise ValueError("oracle_topk_thresholds rejected its arguments")
+        return t
+
+    def topk_mlp(self, x, w_gate, w_up, w_down, k, residual=None):
+        """The top-k variant: row b runs the CATS MLP at its own cutoff
+        t_b = topk_thresholds(x, w_gate, k)[b].  Returns the cats_mlp dict
+        of all rows plus "t" [B]."""
+        x = np.ascontiguousarray(x, dtype=_F)
+        if x.ndim == 1:
+            x = x[None, :]
+        B = x.shape[0]
+        ts = self.topk_thresholds(x, w_gate, k)
+        res = None if residual is None else np.asarray(residual, dtype=_F).reshape(B, -1)
+        rows = [self.cats_mlp(x[b : b + 1], w_gate, w_up, w_down, ts[b],
+                              residual=None if res is None else res[b : b + 1]) for b in range(B)]
+        out = {"y": np.concatenate([r["y"] for r in rows]), "v": np.concatenate([r["v"] for r in rows]),
+               "cnt": np.concatenate([r["cnt"] for r in rows]), "idx": [r["idx"][0] for r in rows],
+               "h": [r["h"][0] for r in rows], "t": ts}
         return out
 
     def sparse_input_gemv(self, x, w, t, residual=None):

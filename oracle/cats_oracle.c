@@ -116,6 +116,30 @@ int oracle_rmsnorm(const float* x, int32_t B, int32_t d, double eps, double* out
   return 0;
 }
 
+int oracle_topk_thresholds(const float* x, int32_t B, int32_t d, int32_t m, const float* w_gate,
+                           double k, double* t_out) {
+  if (!x || !w_gate || !t_out || B <= 0 || d <= 0 || m <= 0 || !(k >= 0.0 && k <= 1.0)) return -1;
+  const int64_t r = oracle_cutoff_rank(m, k);
+  double* a = (double*)malloc(sizeof(double) * (size_t)m);
+  if (!a) return -1;
+  for (int32_t b = 0; b < B; ++b) {
+    if (r == 0) {
+      t_out[b] = 0.0;
+      continue;
+    }
+    if (oracle_calib_acts(x + (size_t)b * d, 1, d, m, w_gate, a) != 0) {
+      free(a);
+      return -1;
+    }
+    if (oracle_threshold(a, m, k, &t_out[b]) != 0) {
+      free(a);
+      return -1;
+    }
+  }
+  free(a);
+  return 0;
+}
+
 int oracle_sparse_input_gemv(const float* x, int32_t B, int32_t d, int32_t n, const float* w,
                              double t_in, const float* residual, double* y, int32_t* active_idx,
                              int32_t* active_cnt) {

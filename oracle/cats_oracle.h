@@ -59,6 +59,16 @@ int oracle_cats_mlp(const float* x, int32_t B, int32_t d, int32_t m,
  * the sum of squares taken in ascending i. */
 int oracle_rmsnorm(const float* x, int32_t B, int32_t d, double eps, double* out);
 
+/* Per-token cutoffs for a top-k variant of CATS (the paper's future work:
+ * a minimum sparsity per token instead of one calibrated t): for every row
+ * b, v_j = SiLU(x_b . Wg[:, j]) over the m neurons and
+ *   t_out[b] = the r-th smallest |v_j| (1-indexed), r = oracle_cutoff_rank(m, k)
+ * i.e. Eq. 3 applied to the token's own m activations.  CATS with t_out[b]
+ * on row b then keeps the neurons with |v_j| >= t_out[b]: at least m - r + 1
+ * of them (ties kept).  k = 0 gives 0.  Returns 0, or -1 on a bad argument. */
+int oracle_topk_thresholds(const float* x, int32_t B, int32_t d, int32_t m, const float* w_gate,
+                           double k, double* t_out);
+
 /* CATS on the input of a linear layer (Appendix B wraps the attention
  * block's input x in CATS_t): y_b = residual_b + CATS_t(x_b) W with
  * CATS_t(z) = z where |z| >= t, else 0 (Eq. 4).  W is [d x n] row-major, row

@@ -32,6 +32,8 @@ What pins what:
   sparse_input_gemv      Appendix B's CATS on a layer input: masked product
                          vs numpy, t = 0 plain product, t above all |x| is
                          zero, one kept channel exact, ties kept
+  topk_thresholds        per-token cutoffs: each row's own order statistic
+                         vs a numpy sort, exact kept counts, k = 0 and 1
 """
 from __future__ import annotations
 
@@ -392,6 +394,30 @@ def pin_sparse_input_gemv(O):
     assert tie["cnt"][0] == 1
 
 
+def pin_topk_thresholds(O):
+    """Top-k variant: every row's cutoff is its own order statistic of
+    |SiLU(x W_gate)| (numpy float64 sort), the rows differ, the kept count
+    obeys #{|v| >= t_b} >= m - r + 1 with equality when values are distinct,
+    k = 0 gives 0, k = 1 keeps the largest only."""
+    r_ = np.random.default_rng(20)
+    B, d, m = 4, 24, 37
+    x = (r_.standard_normal((B, d)) * np.array([[0.3], [1.0], [2.0], [4.0]])).astype(np.float32)
+    wg = (r_.standard_normal((d, m)) * 0.3).astype(np.float32)
+    a = np.abs(_np_silu(x.astype(np.float64) @ wg.astype(np.float64)))
+    for k in (0.25, 0.5, 0.9, 1.0):
+        t = O.topk_thresholds(x, wg, k)
+        rr = _rank(m, k)
+        for b in range(B):
+            exp = np.sort(a[b])[rr - 1]
+            assert abs(t[b] - exp) <= _tol(O, 2e-6, 1e-13) * max(1.0, exp), (k, b, t[b], exp)
+            ours = O.calib_acts(x[b : b + 1], wg)[0]
+            assert int(np.sum(ours >= t[b])) == m - rr + 1, (k, b)
+        assert len(set(np.round(t, 9))) > 1, "rows of different scale share a cutoff"
+    assert not O.topk_thresholds(x, wg, 0.0).any()
+    full = O.topk_mlp(x, wg, wg, wg.T.copy(), 0.5)
+    assert np.array_equal(full["cnt"], np.full(B, m - _rank(m, 0.5) + 1))
+
+
 ALL_PINS = [
     pin_silu_closed_forms,
     pin_dense_vs_library,
@@ -409,4 +435,5 @@ ALL_PINS = [
     pin_stack_vs_library,
     pin_stack_infinite_t_is_identity,
     pin_sparse_input_gemv,
+    pin_topk_thresholds,
 ]

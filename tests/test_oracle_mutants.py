@@ -53,6 +53,9 @@ MUTANTS = {
     # input sparsity: W read transposed
     "gemv_transposed": ("for (int32_t k = 0; k < n; ++k) s[k] += xc * (real)w_row[k];",
                         "for (int32_t k = 0; k < n; ++k) s[k] += xc * (real)w[((size_t)k * d + i) % ((size_t)d * n)];"),
+    # top-k: one cutoff computed from row 0 used for every row
+    "topk_row0": ("if (oracle_calib_acts(x + (size_t)b * d, 1, d, m, w_gate, a) != 0) {",
+                  "if (oracle_calib_acts(x, 1, d, m, w_gate, a) != 0) {"),
     # v reported before the activation
     "v_before_silu": ("if (v_all) v_all[(size_t)b * m + j] = (double)v;",
                       "if (v_all) v_all[(size_t)b * m + j] = (double)g[j];"),
