@@ -25,6 +25,7 @@ from __future__ import annotations
 import argparse
 import ctypes
 import json
+import math
 import os
 import sys
 import time
@@ -263,6 +264,43 @@ def bench_sparse_input(P, W, torch, timed, steps, warm, rotate):
     return out
 
 
+def bench_topk(P, W, torch, timed, layers, xs, ks, dense_us, steps, warm):
+    """Per-token top-k variant on the benchmark layer: row b keeps the
+    neurons at or above the r-th smallest of its own |v| (r = ceil(k m)),
+    one token per call, weight copies rotated as for the calibrated path."""
+    L = P.raw()
+    dev = xs.device
+    R, ntok = len(layers), xs.shape[0]
+    d, m = layers[0].d, layers[0].m
+    nb = int(L.cats_topk_workspace_bytes(d, m, 1))
+    ws = torch.zeros(nb, dtype=torch.uint8, device=dev)
+    y = torch.empty((1, d), dtype=torch.float32, device=dev)
+    tb = torch.empty((1,), dtype=torch.float32, device=dev)
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    xptr = [ctypes.c_void_p(xs[i : i + 1].data_ptr()) for i in range(ntok)]
+    yptr, tptr, wsp = ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(tb.data_ptr()), ctypes.c_void_p(ws.data_ptr())
+
+    def call(s, k):
+        st = L.cats_mlp_forward_topk(layers[s % R].c, xptr[s % ntok], 1, float(k), None, yptr, None, wsp, nb,
+                                     stream, tptr)
+        if st != 0:
+            raise P.CatsError(st, L.cats_last_error().decode())
+
+    out = {"workload": "per-token top-k on the benchmark layer, batch 1", "steps": steps}
+    for k in ks:
+        ms = timed(lambda s, k=k: call(s, k), warm, steps)
+        kept = m - max(1, math.ceil(k * m - 1e-6)) + 1
+        out[str(k)] = {"us": round(ms * 1e3 / steps, 3), "kept": kept,
+                       "speedup_vs_dense": round(dense_us / (ms * 1e3 / steps), 3)}
+    P.timer_reset()
+    P.timer_enable(True)
+    timed(lambda s: call(s, ks[0]), 0, 32)
+    P.timer_enable(False)
+    out[f"kernel_avg_us_k{ks[0]}"] = {n: round(v[1] * 1e3 / max(1, v[0]), 3)
+                                      for n, v in P.timer_read().items() if v[0]}
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -284,8 +322,8 @@ def main() -> int:
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: the CATS MLP hot path has no multi-GPU "
-              "path in this build (see DESIGN.md for how it would shard); run with --gpus 1",
+        print("bench.py measures one GPU: the CATS MLP hot path runs on a single GPU "
+              "(no collectives); run with --gpus 1",
               file=sys.stderr)
         return 2
 
@@ -462,6 +500,8 @@ def main() -> int:
         }
         out["kernel_avg_us"] = {n: round(v[1] * 1e3 / max(1, v[0]), 3) for n, v in kt.items()}
         out["timed_region_with_kernel_events_ms_per_step"] = round(ms_timer / K, 5)
+        out["topk"] = bench_topk(P, W, torch, timed, layers, xs, ks, dense_us, K, Wm)
+        log(f"[bench] top-k: {out['topk']}")
 
     if not args.no_extras and not args.no_stacks:
         del layers, base

@@ -192,6 +192,24 @@ cats_status cats_stack_forward(const cats_layer* layers, int32_t L, const float*
                                float* x_all, const cats_forward_aux* aux, void* ws,
                                size_t ws_bytes, void* stream);
 
+/* Per-token top-k variant of the forward (the appendix comparing target and
+ * actual sparsity suggests enforcing the target sparsity per layer at
+ * inference as future work): row b keeps the neurons with
+ * |v_bj| >= t_b, where t_b is the r-th smallest of its own m values |v_b.|,
+ * r = ceil(sparsity * m - 1e-6) clamped to [1, m] (Eq. 3 over one token);
+ * sparsity = 0 keeps every neuron.  Each row keeps at least m - r + 1
+ * neurons (ties at t_b are kept).  Three steps on `stream`: the gate
+ * activations of all rows, an exact per-row radix select, and the fused
+ * forward reading those activations (W_gate is read once).  Arguments as
+ * cats_mlp_forward; t_out: dev [B] fp32 receiving t_b, or NULL.  Rows are
+ * processed in passes of at most 8 (the vector-ALU kernel).  Workspace:
+ * cats_topk_workspace_bytes(d, m, B).  Enqueue only. */
+size_t cats_topk_workspace_bytes(int32_t d, int32_t m, int32_t max_batch);
+cats_status cats_mlp_forward_topk(const cats_layer* layer, const float* x, int32_t B,
+                                  double sparsity, const float* residual, float* y,
+                                  const cats_forward_aux* aux, void* ws, size_t ws_bytes,
+                                  void* stream, float* t_out);
+
 /* CATS on the input of a linear layer.  Appendix B wraps each attention
  * block's input in CATS_t, so its query / key / value projections take a
  * sparse input:

@@ -18,6 +18,7 @@ from ._lib import (  # noqa: F401
     lib_path,
     mlp_dense,
     mlp_forward,
+    mlp_forward_topk,
     pack_weights,
     raw,
     Stack,

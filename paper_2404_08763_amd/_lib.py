@@ -73,6 +73,9 @@ _SIGNATURES = {
     "cats_sparse_input_workspace_bytes": ([_i32, _i32, _i32], _sz),
     "cats_sparse_input_gemv": ([_vp, _i32, _i32, _i32, _vp, _i32, _f32, _vp, _vp, ctypes.POINTER(_Aux), _vp,
                                 _sz, _vp], _i32),
+    "cats_topk_workspace_bytes": ([_i32, _i32, _i32], _sz),
+    "cats_mlp_forward_topk": ([ctypes.POINTER(_Layer), _vp, _i32, _f64, _vp, _vp, ctypes.POINTER(_Aux), _vp, _sz,
+                               _vp, _vp], _i32),
     "cats_rmsnorm": ([_vp, _vp, _i32, _i32, _f32, _vp], _i32),
     "cats_timer_enable": ([_i32], _i32),
     "cats_timer_reset": ([], _i32),
@@ -269,6 +272,41 @@ def mlp_forward(layer: Layer, x: torch.Tensor, t: float, residual: Optional[torc
     if aux:
         return out, bufs
     return out
+
+
+def mlp_forward_topk(layer: Layer, x: torch.Tensor, sparsity: float, residual: Optional[torch.Tensor] = None,
+                     out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, aux: bool = False):
+    """Per-token top-k variant.  Returns (y, t [B]) or (y, t, aux dict)."""
+    _dev(x, "x", torch.float32)
+    B = _rows(x)
+    if out is None:
+        out = torch.empty_like(x)
+    _dev(out, "out", torch.float32)
+    if residual is not None:
+        _dev(residual, "residual", torch.float32)
+    if ws is None:
+        nbytes = int(raw().cats_topk_workspace_bytes(layer.d, layer.m, B))
+        if nbytes == 0:
+            raise ValueError("arguments outside the supported range")
+        ws = torch.zeros(nbytes, dtype=torch.uint8, device=x.device)
+    t = torch.empty((B,), dtype=torch.float32, device=x.device)
+    aux_c = None
+    bufs = None
+    if aux:
+        m = layer.m
+        bufs = {
+            "idx": torch.empty((B, m), dtype=torch.int32, device=x.device),
+            "cnt": torch.empty((B,), dtype=torch.int32, device=x.device),
+            "v": torch.empty((B, m), dtype=torch.float32, device=x.device),
+            "h": torch.empty((B, m), dtype=torch.float32, device=x.device),
+        }
+        aux_c = _Aux(bufs["idx"].data_ptr(), bufs["cnt"].data_ptr(), bufs["v"].data_ptr(), bufs["h"].data_ptr())
+    _check(raw().cats_mlp_forward_topk(layer.c, _ptr(x), B, float(sparsity), _ptr(residual), _ptr(out),
+                                       ctypes.byref(aux_c) if aux_c is not None else None, _ptr(ws), ws.numel(),
+                                       _stream(), _ptr(t)))
+    if aux:
+        return out, t, bufs
+    return out, t
 
 
 def mlp_dense(layer: Layer, x: torch.Tensor, residual: Optional[torch.Tensor] = None,

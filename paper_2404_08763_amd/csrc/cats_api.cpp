@@ -136,7 +136,8 @@ int batch_tile(int rows) {
 // norm: x is RMSNorm'ed (unit gain, eps) inside the fused kernel first.
 cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, bool dense,
                     const float* residual, float* y, const cats_forward_aux* aux, void* ws,
-                    size_t ws_bytes, void* stream, bool norm = false, float eps = 0.f) {
+                    size_t ws_bytes, void* stream, bool norm = false, float eps = 0.f,
+                    const float* vin = nullptr, const float* vin_t = nullptr) {
   cats_status st = check_layer(L);
   if (st != CATS_OK) return st;
   if (!x || !y) return fail(CATS_ERR_NULL, "x or y is NULL");
@@ -164,7 +165,7 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
   char* w = static_cast<char*>(ws);
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const int G = cats::fused_grid(m);
-  if (bf16 && B >= cats::kBatchedMinRows && cats::batched_ks(d) > 0) {
+  if (!vin && bf16 && B >= cats::kBatchedMinRows && cats::batched_ks(d) > 0) {
     // all rows in one pass: gate/up on the matrix cores, down by column tiles
     cats::BatchedArgs ba;
     ba.wg = L->w_gate_t;
@@ -234,6 +235,8 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
     fa.t = dense ? 0.f : t;
     fa.norm = norm ? 1 : 0;
     fa.eps = eps;
+    fa.vin = vin ? vin + (size_t)b0 * m : nullptr;
+    fa.vin_t = vin_t ? vin_t + b0 : nullptr;
     fa.partial = reinterpret_cast<float*>(w + lay.partial);
     fa.aux = want_aux ? 1 : 0;
     fa.seg_j = reinterpret_cast<int*>(w + lay.seg_j);
@@ -243,7 +246,10 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
     fa.seg_cnt = reinterpret_cast<int*>(w + lay.seg_cnt);
     const int bt = batch_tile(bp);
     hipError_t e;
-    if (bf16)
+    if (vin)
+      e = bf16 ? cats::launch_fused_bf16_topk(nch, bt, fa.aux != 0, fa, G, s)
+               : cats::launch_fused_f32_topk(nch, bt, fa.aux != 0, fa, G, s);
+    else if (bf16)
       e = dense ? cats::launch_fused_bf16_dense(nch, bt, fa, G, s)
           : fa.aux ? cats::launch_fused_bf16_cats_aux(nch, bt, fa, G, s)
                    : cats::launch_fused_bf16_cats(nch, bt, fa, G, s);
@@ -773,6 +779,56 @@ cats_status cats_calibrate_stack(const cats_layer* layers, int32_t L, const floa
       st = run_mlp(ly, XN + (size_t)r0 * d, nb, 0.f, true, xr, xr, nullptr, ws, general, stream);
       if (st != CATS_OK) return fail(st, "layer %d propagation: %s", l, g_last_error.c_str());
     }
+  }
+  return CATS_OK;
+}
+
+size_t cats_topk_workspace_bytes(int32_t d, int32_t m, int32_t max_batch) {
+  const size_t base = round_up(cats_workspace_bytes(d, m, max_batch, 0), kAlign);
+  if (base == 0) return 0;
+  return base + round_up((size_t)max_batch * m * sizeof(float), kAlign) +
+         round_up((size_t)max_batch * sizeof(float), kAlign);
+}
+
+cats_status cats_mlp_forward_topk(const cats_layer* layer, const float* x, int32_t B, double sparsity,
+                                  const float* residual, float* y, const cats_forward_aux* aux, void* ws,
+                                  size_t ws_bytes, void* stream, float* t_out) {
+  cats_status st = check_layer(layer);
+  if (st != CATS_OK) return st;
+  if (!x || !y) return fail(CATS_ERR_NULL, "x or y is NULL");
+  if (B < 1 || B > CATS_MAX_BATCH) return fail(CATS_ERR_SHAPE, "B=%d outside [1, %d]", (int)B, CATS_MAX_BATCH);
+  if (!std::isfinite(sparsity) || sparsity < 0.0 || sparsity > 1.0)
+    return fail(CATS_ERR_RANGE, "sparsity must be in [0, 1]");
+  if (!aligned(x, 16) || !aligned(y, 16) || (residual && !aligned(residual, 16)))
+    return fail(CATS_ERR_ALIGN, "x, y and residual must be 16-byte aligned");
+  if (t_out && !aligned(t_out, 4)) return fail(CATS_ERR_ALIGN, "t_out must be 4-byte aligned");
+  if (aux && ((aux->active_idx && !aligned(aux->active_idx, 4)) || (aux->active_cnt && !aligned(aux->active_cnt, 4)) ||
+              (aux->active_v && !aligned(aux->active_v, 4)) || (aux->active_h && !aligned(aux->active_h, 4))))
+    return fail(CATS_ERR_ALIGN, "aux outputs must be 4-byte aligned");
+  const int d = layer->d, m = layer->m;
+  const int bf16 = layer->wdtype == CATS_BF16;
+  const size_t base = round_up(cats_workspace_bytes(d, m, B, 0), kAlign);
+  st = check_ws(ws, ws_bytes, cats_topk_workspace_bytes(d, m, B));
+  if (st != CATS_OK) return st;
+  float* vbuf = reinterpret_cast<float*>(static_cast<char*>(ws) + base);
+  float* tbuf = reinterpret_cast<float*>(static_cast<char*>(ws) + base + round_up((size_t)B * m * sizeof(float), kAlign));
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nch = cats::fused_nch(bf16, d);
+  const int bt_max = cats::fused_bt_max(bf16, nch);
+  const int G = cats::fused_grid(m);
+  for (int b0 = 0; b0 < B; b0 += bt_max) {
+    const int bp = (B - b0) < bt_max ? (B - b0) : bt_max;
+    hipError_t e = cats::launch_gate_v(bf16, nch, batch_tile(bp), x + (size_t)b0 * d, layer->w_gate_t, bp, d, m,
+                                       vbuf + (size_t)b0 * m, G, s);
+    if (e != hipSuccess) return hip_fail(e, "gate activation launch");
+  }
+  hipError_t e = cats::launch_row_select(vbuf, B, m, cutoff_rank(m, sparsity), tbuf, s);
+  if (e != hipSuccess) return hip_fail(e, "per-row cutoff launch");
+  st = run_mlp(layer, x, B, 0.f, false, residual, y, aux, ws, base, stream, false, 0.f, vbuf, tbuf);
+  if (st != CATS_OK) return st;
+  if (t_out) {
+    e = hipMemcpyAsync(t_out, tbuf, (size_t)B * sizeof(float), hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "cutoff copy");
   }
   return CATS_OK;
 }

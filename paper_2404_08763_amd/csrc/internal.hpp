@@ -38,6 +38,8 @@ struct FusedArgs {
   float t;
   int norm;            // RMSNorm x (unit gain) before the block
   float eps;           // its epsilon
+  const float* vin;    // top-k variant: v [B x m] computed beforehand
+  const float* vin_t;  // and one cutoff per row [B]
   float* partial;      // [G x B x d]
   int aux;             // write the union segments for the aux outputs
   int* seg_j;          // [m]
@@ -149,6 +151,15 @@ hipError_t launch_fused_f32_cats(int nch, int bt, const FusedArgs& a, int G, hip
 hipError_t launch_fused_f32_cats_aux(int nch, int bt, const FusedArgs& a, int G, hipStream_t s);
 hipError_t launch_fused_f32_dense(int nch, int bt, const FusedArgs& a, int G, hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
+
+// Top-k variant: gate activations of B <= 8 rows into v [B x m], the per-row
+// cutoffs (rank r of |v| within each row) into t [B], then the fused kernel
+// reading v and t (no W_gate row).
+hipError_t launch_gate_v(int wdtype_bf16, int nch, int bt, const float* x, const void* wg, int B,
+                         int d, int m, float* v, int G, hipStream_t s);
+hipError_t launch_row_select(const float* v, int B, int m, int64_t r, float* t, hipStream_t s);
+hipError_t launch_fused_bf16_topk(int nch, int bt, bool aux, const FusedArgs& a, int G, hipStream_t s);
+hipError_t launch_fused_f32_topk(int nch, int bt, bool aux, const FusedArgs& a, int G, hipStream_t s);
 
 // k-steps of the batched gate/up kernel for width d (0: no instantiation
 // covers d exactly; those widths use the fused kernel).

@@ -40,7 +40,9 @@
 
 namespace cats {
 
-template <typename WT, int NCH, int BT, bool DENSE, bool AUX>
+// VIN: the gate activations v (and one threshold per row) come precomputed
+// (the per-token top-k variant); no W_gate row is read.
+template <typename WT, int NCH, int BT, bool DENSE, bool AUX, bool VIN>
 __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs a) {
   typedef typename wtraits<WT>::elem E;
   constexpr int VEC = wtraits<WT>::VEC;
@@ -66,6 +68,10 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
   const int w = __builtin_amdgcn_readfirstlane(tid / kWaveSize);
   const int B = a.B, d = a.d, m = a.m;
   const float t = a.t;
+  // per-row cutoffs of the top-k variant (every row uses t otherwise)
+  float trow[BT];
+#pragma unroll
+  for (int b = 0; b < BT; ++b) trow[b] = (VIN && b < B) ? a.vin_t[b] : t;
   const uint32_t row_bytes = (uint32_t)d * sizeof(E);
   const uint32_t mat_bytes = (uint32_t)((uint64_t)m * row_bytes);
   const __amdgpu_buffer_rsrc_t rg = make_rsrc(a.wg, mat_bytes);
@@ -145,7 +151,7 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
       const bool ok = (NV % NT == 0 || i4 < NV) && b < B && c < d;
       xv[k] = ld_buf16(rx, ok ? (uint32_t)((b * d + c) * sizeof(float)) : kOOB);
     }
-    load_row(gA, rg, row_base(0 < ni, n0 + w));
+    if constexpr (!VIN) load_row(gA, rg, row_base(0 < ni, n0 + w));
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int i4 = tid + k * NT;
@@ -186,19 +192,28 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
   // up(i); finish up(i-1).
   auto iter = [&](int i, u32x4(&gcur)[NCH], u32x4(&gnxt)[NCH], u32x4(&ucur)[NCH],
                   u32x4(&uprev)[NCH]) {
-    load_row(gnxt, rg, row_base(i + 1 < ni, n0 + w + (i + 1) * W));
+    if constexpr (!VIN) load_row(gnxt, rg, row_base(i + 1 < ni, n0 + w + (i + 1) * W));
     uint32_t mask = 0;
     float v[BT];
 #pragma unroll
     for (int b = 0; b < BT; ++b) v[b] = 0.f;
     if (i < ni) {
-      float g[BT];
-      row_dot(gcur, g);
+      if constexpr (VIN) {
+        const int j = n0 + w + i * W;
+#pragma unroll
+        for (int b = 0; b < BT; ++b)
+          if (b < B) v[b] = a.vin[(size_t)b * m + j];
+      } else {
+        float g[BT];
+        row_dot(gcur, g);
+#pragma unroll
+        for (int b = 0; b < BT; ++b)
+          if (b < B) v[b] = silu(g[b]);
+      }
 #pragma unroll
       for (int b = 0; b < BT; ++b) {
         if (b < B) {
-          v[b] = silu(g[b]);
-          const bool keep = DENSE || !(fabsf(v[b]) < t);
+          const bool keep = DENSE || !(fabsf(v[b]) < trow[b]);
           mask |= (uint32_t)keep << b;
         }
       }
@@ -363,23 +378,23 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
 
 // Launch one instantiation; NCH and the batch tile are compile-time, so the
 // host picks them from d and B (see fused_nch / fused_bt_max).
-template <typename WT, bool DENSE, bool AUX, int NCH>
+template <typename WT, bool DENSE, bool AUX, bool VIN, int NCH>
 hipError_t launch_fused_nch(int bt, const FusedArgs& a, int G, hipStream_t s) {
   constexpr int DP = NCH * kWaveSize * wtraits<WT>::VEC;
   const dim3 grid(G), block(kFusedWaves * kWaveSize);
-  KernelTimer timer(DENSE ? "mlp_fused_dense" : "mlp_fused_cats", s);
+  KernelTimer timer(VIN ? "mlp_fused_topk" : (DENSE ? "mlp_fused_dense" : "mlp_fused_cats"), s);
   switch (bt) {
-    case 1: hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 1, DENSE, AUX>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
-    case 2: hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 2, DENSE, AUX>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
+    case 1: hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 1, DENSE, AUX, VIN>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
+    case 2: hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 2, DENSE, AUX, VIN>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
     case 4:
       if constexpr (4 * DP * 4 <= kXLdsBytes) {
-        hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 4, DENSE, AUX>), grid, block, 0, s, timer.start(), timer.stop(), 0, a);
+        hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 4, DENSE, AUX, VIN>), grid, block, 0, s, timer.start(), timer.stop(), 0, a);
         break;
       }
       return hipErrorInvalidValue;
     case 8:
       if constexpr (8 * DP * 4 <= kXLdsBytes) {
-        hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 8, DENSE, AUX>), grid, block, 0, s, timer.start(), timer.stop(), 0, a);
+        hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 8, DENSE, AUX, VIN>), grid, block, 0, s, timer.start(), timer.stop(), 0, a);
         break;
       }
       return hipErrorInvalidValue;
@@ -388,15 +403,15 @@ hipError_t launch_fused_nch(int bt, const FusedArgs& a, int G, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <typename WT, bool DENSE, bool AUX>
+template <typename WT, bool DENSE, bool AUX, bool VIN = false>
 hipError_t launch_fused_t(int nch, int bt, const FusedArgs& a, int G, hipStream_t s) {
   switch (nch) {
-    case 1: return launch_fused_nch<WT, DENSE, AUX, 1>(bt, a, G, s);
-    case 2: return launch_fused_nch<WT, DENSE, AUX, 2>(bt, a, G, s);
-    case 4: return launch_fused_nch<WT, DENSE, AUX, 4>(bt, a, G, s);
-    case 8: return launch_fused_nch<WT, DENSE, AUX, 8>(bt, a, G, s);
-    case 10: return launch_fused_nch<WT, DENSE, AUX, 10>(bt, a, G, s);
-    case 16: return launch_fused_nch<WT, DENSE, AUX, 16>(bt, a, G, s);
+    case 1: return launch_fused_nch<WT, DENSE, AUX, VIN, 1>(bt, a, G, s);
+    case 2: return launch_fused_nch<WT, DENSE, AUX, VIN, 2>(bt, a, G, s);
+    case 4: return launch_fused_nch<WT, DENSE, AUX, VIN, 4>(bt, a, G, s);
+    case 8: return launch_fused_nch<WT, DENSE, AUX, VIN, 8>(bt, a, G, s);
+    case 10: return launch_fused_nch<WT, DENSE, AUX, VIN, 10>(bt, a, G, s);
+    case 16: return launch_fused_nch<WT, DENSE, AUX, VIN, 16>(bt, a, G, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -250,6 +250,27 @@ def test_sparse_input_validation():
     assert call(ws=0) == WORKSPACE and call(ws_bytes=need - 1) == WORKSPACE
 
 
+def test_topk_validation():
+    L = P.raw()
+    need = L.cats_topk_workspace_bytes(64, 96, 2)
+    assert need >= P.workspace_bytes(64, 96, 2, 0) + 2 * 96 * 4
+    assert L.cats_topk_workspace_bytes(0, 96, 1) == 0 and L.cats_topk_workspace_bytes(64, 96, 17) == 0
+
+    def call(layer=None, x=A + 65536, B=2, k=0.5, res=None, y=A * 2, ws=A * 4, ws_bytes=need, t_out=None):
+        lay = _layer() if layer is None else layer
+        return L.cats_mlp_forward_topk(ctypes.byref(lay), ctypes.c_void_p(x) if x else None, B, k,
+                                       ctypes.c_void_p(res) if res else None, ctypes.c_void_p(y) if y else None,
+                                       None, ctypes.c_void_p(ws) if ws else None, ws_bytes, None,
+                                       ctypes.c_void_p(t_out) if t_out else None)
+
+    assert call(x=0) == NULL and call(y=0) == NULL
+    assert call(B=0) == SHAPE and call(B=17) == SHAPE
+    assert call(k=-0.1) == RANGE and call(k=1.01) == RANGE and call(k=math.nan) == RANGE
+    assert call(x=A + 4) == ALIGN and call(y=A + 4) == ALIGN and call(res=A + 8) == ALIGN
+    assert call(t_out=A + 2) == ALIGN
+    assert call(ws=0) == WORKSPACE and call(ws_bytes=need - 1) == WORKSPACE
+
+
 def test_forward_workspace_is_workspace_bytes():
     """The forward accepts exactly cats_workspace_bytes(d, m, B, 0) and up."""
     for B in (1, 3, 8, 16):

@@ -1,0 +1,148 @@
+"""Per-token top-k variant on the device against the CPU oracle.
+
+Row b keeps the neurons with |v_bj| >= t_b, t_b the r-th smallest of its
+own |v_b.| (r = ceil(k m), Eq. 3 over one token).  Bars:
+  - t_b within 1e-3 t_b of the oracle's, and a valid r-th order statistic
+    of the oracle's |v_b.| at that tolerance;
+  - the device's own choice is exact: its smallest kept |v| is t_b and the
+    number of its |v| below t_b is under r, at or above r - (ties at t_b);
+  - per row, the single-block bars at the oracle's t_b (active sets equal
+    outside the band, y within 2e-2 ||y||_inf, 1e-4 once reconciled).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2404_08763_amd as P
+from paper_2404_08763_amd import workloads as W
+
+from gpu_util import BAND, check_forward, device_layer, host_f32, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a device"
+    return torch.device("cuda:0")
+
+
+def _rank(m, k):
+    if k == 0.0:
+        return 0
+    return min(m, max(1, math.ceil(k * m - 1e-6)))
+
+
+def _check(O, layer, hw, x, k, label, residual=None):
+    B, m = x.shape[0], hw[0].shape[1]
+    xd = torch.from_numpy(x).cuda()
+    rd = None if residual is None else torch.from_numpy(residual).cuda()
+    y, tg, aux = P.mlp_forward_topk(layer, xd, k, residual=rd, aux=True)
+    tg = tg.cpu().numpy().astype(np.float64)
+    ref = O.topk_mlp(x, *hw, k, residual=residual)
+    r = _rank(m, k)
+    cnt = aux["cnt"].cpu().numpy()
+    idx = aux["idx"].cpu().numpy()
+    va = np.abs(aux["v"].cpu().numpy())
+    flips = 0
+    for b in range(B):
+        to = float(ref["t"][b])
+        # the device's selection is exact on its own values
+        n = int(cnt[b])
+        if r == 0:
+            assert tg[b] == 0.0 and n == m, (label, b)
+        else:
+            kept = va[b, :n]
+            assert float(kept.min()) == tg[b], (label, b, float(kept.min()), tg[b])
+            ties = int((kept == tg[b]).sum())
+            below = m - n
+            assert below < r <= below + ties, (label, b, below, r, ties)
+            # and agrees with the oracle's order statistic
+            assert abs(tg[b] - to) <= 1e-3 * to, (label, b, tg[b], to)
+            a = np.sort(np.abs(ref["v"][b]))
+            lo = int(np.searchsorted(a, tg[b] * (1 - BAND), side="left"))
+            hi = int(np.searchsorted(a, tg[b] * (1 + BAND), side="right"))
+            assert lo < r <= hi, (label, b, lo, r, hi)
+        # the block itself at the oracle's cutoff
+        refb = {"y": ref["y"][b : b + 1], "v": ref["v"][b : b + 1], "idx": [ref["idx"][b]], "h": [ref["h"][b]]}
+        rall = O.cats_mlp(x[b : b + 1], *hw, t=0.0, residual=None if residual is None else residual[b : b + 1])
+        auxb = {kk: aux[kk][b : b + 1] for kk in ("idx", "cnt", "v", "h")}
+        res = check_forward(y[b : b + 1], auxb, refb, to, 1, f"{label} row {b}", ref_all=rall, w_down=hw[2])
+        flips += res["band_flips"]
+    print(f"[topk] {label}: t {np.round(tg[:4], 5)} kept {cnt[:4]} of {m}; {flips} band flips")
+
+
+def _x(B, d, seed=21, scale=1.0):
+    g = torch.Generator().manual_seed(seed)
+    return (torch.randn((B, d), generator=g) * scale).numpy()
+
+
+@pytest.fixture(scope="module")
+def small_bf16(dev):
+    d, m = 1032, 693
+    wg, wu, wd = W.weights(d, m, torch.bfloat16, layer=3)
+    return device_layer(wg, wu, wd), host_f32(wg, wu, wd)
+
+
+@pytest.fixture(scope="module")
+def small_f32(dev):
+    c = W.CONFIGS["C1"]
+    wg, wu, wd = W.weights(c.d, c.m, c.wdtype)
+    return device_layer(wg, wu, wd), host_f32(wg, wu, wd)
+
+
+@pytest.mark.parametrize("k", [0.0, 0.5, 0.9, 1.0])
+@pytest.mark.parametrize("B", [1, 3, 11])
+def test_topk_small_bf16(small_bf16, oracle32, B, k):
+    """Ragged d and m (several neuron tiles and a partial one), rows in one
+    pass and in two (11 rows), the edge sparsities 0 (every neuron) and 1
+    (only the largest |v| and its ties)."""
+    layer, hw = small_bf16
+    say("topk small bf16 B", B, "k", k)
+    _check(oracle32, layer, hw, _x(B, 1032), k, f"small bf16 B{B} k{k}")
+
+
+@pytest.mark.parametrize("k", [0.3, 0.7])
+def test_topk_small_f32_residual(small_f32, oracle32, k):
+    layer, hw = small_f32
+    B = 5
+    say("topk small f32 B", B, "k", k)
+    res = _x(B, 256, seed=22)
+    _check(oracle32, layer, hw, _x(B, 256, seed=23), k, f"small f32 k{k}", residual=res)
+
+
+def test_topk_rows_independent(small_bf16):
+    """Each row's cutoff depends on that row alone: a row in a batch of 9
+    gives the bits it gives alone."""
+    layer, _ = small_bf16
+    x = torch.from_numpy(_x(9, 1032, seed=24)).cuda()
+    say("topk rows independent")
+    y, t = P.mlp_forward_topk(layer, x, 0.6)
+    for b in (0, 4, 8):
+        yb, tb = P.mlp_forward_topk(layer, x[b : b + 1].contiguous(), 0.6)
+        assert torch.equal(t[b : b + 1].view(torch.int32), tb.view(torch.int32)), b
+        assert torch.equal(y[b : b + 1].view(torch.int32), yb.view(torch.int32)), b
+
+
+@pytest.mark.parametrize("B", [1, 16])
+def test_topk_c2_full(dev, oracle32, B):
+    """The Llama2-7B-shaped block (d=4096, m=11008, bf16) with its
+    outlier-channel inputs, at one row and at 16 (two passes of 8)."""
+    c = W.CONFIGS["C2"]
+    wg, wu, wd = W.weights(c.d, c.m, c.wdtype)
+    layer = device_layer(wg, wu, wd)
+    hw = host_f32(wg, wu, wd)
+    x = W.decode_vectors(c, B).numpy()
+    for k in (0.5, 0.9):
+        say("topk C2 B", B, "k", k)
+        _check(oracle32, layer, hw, x, k, f"C2 B{B} k{k}")
+
+
+def test_topk_rejects_bad_sparsity(small_bf16):
+    layer, _ = small_bf16
+    x = torch.zeros((1, 1032), device="cuda")
+    for k in (-0.1, 1.5, float("nan")):
+        with pytest.raises(P.CatsError):
+            P.mlp_forward_topk(layer, x, k)
