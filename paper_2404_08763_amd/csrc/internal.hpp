@@ -7,47 +7,9 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "fused_params.hpp"
+
 namespace cats {
-
-// Geometry of the fused MLP kernel (build-time tunables): waves per block
-// and the number of blocks, one or two per compute unit of an MI355X.
-#ifndef CATS_FUSED_WAVES
-#define CATS_FUSED_WAVES 8
-#endif
-#ifndef CATS_FUSED_BLOCKS
-#define CATS_FUSED_BLOCKS 256
-#endif
-constexpr int kFusedWaves = CATS_FUSED_WAVES;
-constexpr int kFusedBlocks = CATS_FUSED_BLOCKS;
-// Neurons a fused-kernel block may own (its LDS lists are this long); with
-// kFusedBlocks blocks this bounds m.
-constexpr int kFusedMaxNeurons = 65536 / kFusedBlocks;
-constexpr int kMaxNeurons = kFusedBlocks * kFusedMaxNeurons;
-// LDS bytes the fused kernel may spend on the staged x rows.
-constexpr int kXLdsBytes = 128 * 1024;
-
-// Elements per 64-lane chunk of a weight row (16 bytes per lane).
-inline int chunk_elems(int wdtype_bf16) { return wdtype_bf16 ? 512 : 256; }
-
-struct FusedArgs {
-  const void* wg;      // [m x d] W_gate^T
-  const void* wu;      // [m x d] W_up^T
-  const void* wd;      // [m x d] W_down
-  const float* x;      // [B x d]
-  int B, d, m;
-  float t;
-  int norm;            // RMSNorm x (unit gain) before the block
-  float eps;           // its epsilon
-  const float* vin;    // top-k variant: v [B x m] computed beforehand
-  const float* vin_t;  // and one cutoff per row [B]
-  float* partial;      // [G x B x d]
-  int aux;             // write the union segments for the aux outputs
-  int* seg_j;          // [m]
-  uint32_t* seg_mask;  // [m] bit b = active in row b
-  float* seg_v;        // [B x m]
-  float* seg_h;        // [B x m]
-  int* seg_cnt;        // [G]
-};
 
 // Batched path (bf16 weights, kBatchedMinRows..16 rows): gate and up on
 // the matrix cores, then the down-projection by column tiles.  Below 8 rows
