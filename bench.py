@@ -264,6 +264,70 @@ def bench_sparse_input(P, W, torch, timed, steps, warm, rotate):
     return out
 
 
+def bench_ablation(P, W, torch, timed, cfg_name, steps, warm, rotate, layers=None, thr=None):
+    """The kernel-structure ablation of Appendix D on one block: the fused
+    forward against the paper's structure (separate gate, up and down
+    kernels) with rows found by the mask or by per-block index lists, and
+    the dense forward; one token per call, rotated weight copies."""
+    c = W.CONFIGS[cfg_name]
+    dev = torch.device("cuda:0")
+    ks = sorted(thr) if thr is not None else [k for k in c.sparsities if k > 0]
+    if layers is None:
+        wg, wu, wd = W.weights(c.d, c.m, c.wdtype)
+        base = P.layer_from_math(wg.to(dev), wu.to(dev), wd.to(dev))
+        del wg, wu, wd
+        layers = [base] + [P.Layer(base.w_gate_t.clone(), base.w_up_t.clone(), base.w_down.clone())
+                           for _ in range(rotate - 1)]
+    if thr is None:
+        xcal = W.calib_vectors(c).to(dev)
+        wsc = P.workspace(c.d, c.m, 1, xcal.shape[0] * c.m, device=dev)
+        thr = {k: P.calibrate_threshold(layers[0], xcal, k, ws=wsc) for k in ks}
+        del wsc, xcal
+    R = len(layers)
+    xs = W.decode_vectors(c).to(dev)
+    ntok = xs.shape[0]
+    L = P.raw()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    nb = int(L.cats_unfused_workspace_bytes(c.d, c.m, 1))
+    ws = torch.zeros(nb, dtype=torch.uint8, device=dev)
+    y = torch.empty((1, c.d), dtype=torch.float32, device=dev)
+    xptr = [ctypes.c_void_p(xs[i : i + 1].data_ptr()) for i in range(ntok)]
+    yptr, wsp = ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(ws.data_ptr())
+
+    def chk(st):
+        if st != 0:
+            raise P.CatsError(st, L.cats_last_error().decode())
+
+    def fused(s, t):
+        chk(L.cats_mlp_forward(layers[s % R].c, xptr[s % ntok], 1, ctypes.c_float(t), None, yptr, None, wsp, nb,
+                               stream))
+
+    def unfused(s, t, mode):
+        chk(L.cats_mlp_forward_unfused(layers[s % R].c, xptr[s % ntok], 1, ctypes.c_float(t), mode, None, yptr,
+                                       wsp, nb, stream))
+
+    def dense(s):
+        chk(L.cats_mlp_dense(layers[s % R].c, xptr[s % ntok], 1, None, yptr, wsp, nb, stream))
+
+    out = {"workload": f"{cfg_name}: d={c.d} m={c.m} bf16, batch 1", "steps": steps,
+           "dense_us": round(timed(dense, warm, steps) * 1e3 / steps, 3)}
+    for k in ks:
+        t = thr[k]
+        row = {"fused_us": timed(lambda s: fused(s, t), warm, steps) * 1e3 / steps,
+               "unfused_mask_us": timed(lambda s: unfused(s, t, P.CATS_UNFUSED_MASK), warm, steps) * 1e3 / steps,
+               "unfused_index_us": timed(lambda s: unfused(s, t, P.CATS_UNFUSED_INDEX), warm, steps) * 1e3 / steps}
+        out[str(k)] = {n: round(v, 3) for n, v in row.items()}
+    kt = {}
+    for mode, nme in ((P.CATS_UNFUSED_MASK, "mask"), (P.CATS_UNFUSED_INDEX, "index")):
+        P.timer_reset()
+        P.timer_enable(True)
+        timed(lambda s: unfused(s, thr[ks[0]], mode), 0, 32)
+        P.timer_enable(False)
+        kt[nme] = {n: round(v[1] * 1e3 / max(1, v[0]), 3) for n, v in P.timer_read().items() if v[0]}
+    out[f"kernel_avg_us_k{ks[0]}"] = kt
+    return out
+
+
 def bench_topk(P, W, torch, timed, layers, xs, ks, dense_us, steps, warm):
     """Per-token top-k variant on the benchmark layer: row b keeps the
     neurons at or above the r-th smallest of its own |v| (r = ceil(k m)),
@@ -502,6 +566,9 @@ def main() -> int:
         out["timed_region_with_kernel_events_ms_per_step"] = round(ms_timer / K, 5)
         out["topk"] = bench_topk(P, W, torch, timed, layers, xs, ks, dense_us, K, Wm)
         log(f"[bench] top-k: {out['topk']}")
+        out["ablation_" + cfg.name] = bench_ablation(P, W, torch, timed, cfg.name, K, Wm, R, layers,
+                                                      {k: thr[k] for k in ks})
+        log(f"[bench] kernel-structure ablation {cfg.name}: {out['ablation_' + cfg.name]}")
 
     if not args.no_extras and not args.no_stacks:
         del layers, base
@@ -510,6 +577,10 @@ def main() -> int:
         log(f"[bench] C4 stack: {out['stack_C4']}")
         torch.cuda.empty_cache()
         out["batch_C5"] = bench_batch_c5(P, W, torch, timed, args.batch_steps, 4)
+        torch.cuda.empty_cache()
+        other = "C3" if cfg.name == "C2" else "C2"
+        out["ablation_" + other] = bench_ablation(P, W, torch, timed, other, 80, 20, R)
+        log(f"[bench] kernel-structure ablation {other}: {out['ablation_' + other]}")
         torch.cuda.empty_cache()
         out["sparse_input_QKV"] = bench_sparse_input(P, W, torch, timed, 200, 20, R)
         log(f"[bench] sparse-input QKV: {out['sparse_input_QKV']}")

@@ -210,6 +210,30 @@ cats_status cats_mlp_forward_topk(const cats_layer* layer, const float* x, int32
                                   const cats_forward_aux* aux, void* ws, size_t ws_bytes,
                                   void* stream, float* t_out);
 
+/* The forward in the paper's own kernel structure (Section 4.3 and
+ * Appendix D), for the ablation of how the up and down kernels find their
+ * rows.  Four launches on `stream` per pass of at most 8 rows: the gate
+ * activations v = SiLU(x W_gate) to memory, an up-projection kernel writing
+ * h = v * (x W_up) on the active neurons to memory, a down-projection kernel
+ * into per-block partial sums, and their fixed-order sum (+ residual).
+ *   mode CATS_UNFUSED_MASK:  the up and down kernels visit every neuron and
+ *        load a row only under the mask |v_j| >= t (the algorithm without
+ *        atomic operations); a masked row is never read;
+ *   mode CATS_UNFUSED_INDEX: the gate pass also writes each block's
+ *        ascending list of the neurons active in some row (compacted without
+ *        atomics), and the up and down kernels visit only those.
+ * Both compute exactly what cats_mlp_forward computes (same t semantics,
+ * fp32 accumulation); the fused forward is the product path, this entry
+ * point exists to measure the paper's structure.  Arguments as
+ * cats_mlp_forward (no aux outputs).  Workspace:
+ * cats_unfused_workspace_bytes(d, m, B).  Enqueue only. */
+#define CATS_UNFUSED_MASK 0
+#define CATS_UNFUSED_INDEX 1
+size_t cats_unfused_workspace_bytes(int32_t d, int32_t m, int32_t max_batch);
+cats_status cats_mlp_forward_unfused(const cats_layer* layer, const float* x, int32_t B, float t,
+                                     int32_t mode, const float* residual, float* y, void* ws,
+                                     size_t ws_bytes, void* stream);
+
 /* CATS on the input of a linear layer.  Appendix B wraps each attention
  * block's input in CATS_t, so its query / key / value projections take a
  * sparse input:

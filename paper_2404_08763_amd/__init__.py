@@ -9,6 +9,8 @@ binding.  Build with ``python -m paper_2404_08763_amd.build``.
 """
 from ._lib import (  # noqa: F401
     CATS_BF16,
+    CATS_UNFUSED_INDEX,
+    CATS_UNFUSED_MASK,
     CATS_F32,
     CatsError,
     Layer,
@@ -19,6 +21,7 @@ from ._lib import (  # noqa: F401
     mlp_dense,
     mlp_forward,
     mlp_forward_topk,
+    mlp_forward_unfused,
     pack_weights,
     raw,
     Stack,

@@ -76,6 +76,8 @@ _SIGNATURES = {
     "cats_topk_workspace_bytes": ([_i32, _i32, _i32], _sz),
     "cats_mlp_forward_topk": ([ctypes.POINTER(_Layer), _vp, _i32, _f64, _vp, _vp, ctypes.POINTER(_Aux), _vp, _sz,
                                _vp, _vp], _i32),
+    "cats_unfused_workspace_bytes": ([_i32, _i32, _i32], _sz),
+    "cats_mlp_forward_unfused": ([ctypes.POINTER(_Layer), _vp, _i32, _f32, _i32, _vp, _vp, _vp, _sz, _vp], _i32),
     "cats_rmsnorm": ([_vp, _vp, _i32, _i32, _f32, _vp], _i32),
     "cats_timer_enable": ([_i32], _i32),
     "cats_timer_reset": ([], _i32),
@@ -271,6 +273,34 @@ def mlp_forward(layer: Layer, x: torch.Tensor, t: float, residual: Optional[torc
                                   ws.numel(), _stream()))
     if aux:
         return out, bufs
+    return out
+
+
+CATS_UNFUSED_MASK = 0
+CATS_UNFUSED_INDEX = 1
+_UNFUSED_MODES = {"mask": CATS_UNFUSED_MASK, "index": CATS_UNFUSED_INDEX}
+
+
+def mlp_forward_unfused(layer: Layer, x: torch.Tensor, t: float, mode: str = "mask",
+                        residual: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                        ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The forward in separate gate / up / down kernels; mode "mask" or "index"."""
+    _dev(x, "x", torch.float32)
+    B = _rows(x)
+    if mode not in _UNFUSED_MODES:
+        raise ValueError(f"mode must be one of {sorted(_UNFUSED_MODES)}")
+    if out is None:
+        out = torch.empty_like(x)
+    _dev(out, "out", torch.float32)
+    if residual is not None:
+        _dev(residual, "residual", torch.float32)
+    if ws is None:
+        nbytes = int(raw().cats_unfused_workspace_bytes(layer.d, layer.m, B))
+        if nbytes == 0:
+            raise ValueError("arguments outside the supported range")
+        ws = torch.zeros(nbytes, dtype=torch.uint8, device=x.device)
+    _check(raw().cats_mlp_forward_unfused(layer.c, _ptr(x), B, float(t), _UNFUSED_MODES[mode], _ptr(residual),
+                                          _ptr(out), _ptr(ws), ws.numel(), _stream()))
     return out
 
 

@@ -818,8 +818,14 @@ cats_status cats_mlp_forward_topk(const cats_layer* layer, const float* x, int32
   const int G = cats::fused_grid(m);
   for (int b0 = 0; b0 < B; b0 += bt_max) {
     const int bp = (B - b0) < bt_max ? (B - b0) : bt_max;
-    hipError_t e = cats::launch_gate_v(bf16, nch, batch_tile(bp), x + (size_t)b0 * d, layer->w_gate_t, bp, d, m,
-                                       vbuf + (size_t)b0 * m, G, s);
+    cats::GateVArgs ga{};
+    ga.wg = layer->w_gate_t;
+    ga.x = x + (size_t)b0 * d;
+    ga.B = bp;
+    ga.d = d;
+    ga.m = m;
+    ga.v = vbuf + (size_t)b0 * m;
+    hipError_t e = cats::launch_gate_v(bf16, nch, batch_tile(bp), false, ga, G, s);
     if (e != hipSuccess) return hip_fail(e, "gate activation launch");
   }
   hipError_t e = cats::launch_row_select(vbuf, B, m, cutoff_rank(m, sparsity), tbuf, s);
@@ -829,6 +835,86 @@ cats_status cats_mlp_forward_topk(const cats_layer* layer, const float* x, int32
   if (t_out) {
     e = hipMemcpyAsync(t_out, tbuf, (size_t)B * sizeof(float), hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return hip_fail(e, "cutoff copy");
+  }
+  return CATS_OK;
+}
+
+size_t cats_unfused_workspace_bytes(int32_t d, int32_t m, int32_t max_batch) {
+  const size_t base = round_up(cats_workspace_bytes(d, m, max_batch, 0), kAlign);
+  if (base == 0) return 0;
+  return base + 2 * round_up((size_t)max_batch * m * sizeof(float), kAlign);
+}
+
+cats_status cats_mlp_forward_unfused(const cats_layer* layer, const float* x, int32_t B, float t, int32_t mode,
+                                     const float* residual, float* y, void* ws, size_t ws_bytes, void* stream) {
+  cats_status st = check_layer(layer);
+  if (st != CATS_OK) return st;
+  if (!x || !y) return fail(CATS_ERR_NULL, "x or y is NULL");
+  if (B < 1 || B > CATS_MAX_BATCH) return fail(CATS_ERR_SHAPE, "B=%d outside [1, %d]", (int)B, CATS_MAX_BATCH);
+  if (mode != CATS_UNFUSED_MASK && mode != CATS_UNFUSED_INDEX) return fail(CATS_ERR_RANGE, "unknown mode %d", (int)mode);
+  if (std::isnan(t) || t < 0.f) return fail(CATS_ERR_RANGE, "t must be >= 0 (got %g)", (double)t);
+  if (!aligned(x, 16) || !aligned(y, 16) || (residual && !aligned(residual, 16)))
+    return fail(CATS_ERR_ALIGN, "x, y and residual must be 16-byte aligned");
+  const int d = layer->d, m = layer->m;
+  const int bf16 = layer->wdtype == CATS_BF16;
+  st = check_ws(ws, ws_bytes, cats_unfused_workspace_bytes(d, m, B));
+  if (st != CATS_OK) return st;
+  const bool index = mode == CATS_UNFUSED_INDEX;
+  const size_t base = round_up(cats_workspace_bytes(d, m, B, 0), kAlign);
+  char* w = static_cast<char*>(ws);
+  const FwdLayout lay = fwd_layout(d, m, B);
+  float* vbuf = reinterpret_cast<float*>(w + base);
+  float* hbuf = reinterpret_cast<float*>(w + base + round_up((size_t)B * m * sizeof(float), kAlign));
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nch = cats::fused_nch(bf16, d);
+  const int bt_max = cats::fused_bt_max(bf16, nch);
+  const int G = cats::fused_grid(m);
+  for (int b0 = 0; b0 < B; b0 += bt_max) {
+    const int bp = (B - b0) < bt_max ? (B - b0) : bt_max;
+    const int bt = batch_tile(bp);
+    cats::GateVArgs ga{};
+    ga.wg = layer->w_gate_t;
+    ga.x = x + (size_t)b0 * d;
+    ga.B = bp;
+    ga.d = d;
+    ga.m = m;
+    ga.v = vbuf;
+    ga.t = t;
+    ga.seg_j = reinterpret_cast<int*>(w + lay.seg_j);
+    ga.seg_mask = reinterpret_cast<uint32_t*>(w + lay.seg_mask);
+    ga.seg_cnt = reinterpret_cast<int*>(w + lay.seg_cnt);
+    hipError_t e = cats::launch_gate_v(bf16, nch, bt, index, ga, G, s);
+    if (e != hipSuccess) return hip_fail(e, "gate launch");
+    cats::UnfusedArgs ua{};
+    ua.wu = layer->w_up_t;
+    ua.wd = layer->w_down;
+    ua.x = ga.x;
+    ua.v = vbuf;
+    ua.t = t;
+    ua.B = bp;
+    ua.d = d;
+    ua.m = m;
+    ua.seg_j = ga.seg_j;
+    ua.seg_cnt = ga.seg_cnt;
+    ua.h = hbuf;
+    ua.partial = reinterpret_cast<float*>(w + lay.partial);
+    e = cats::launch_unfused_up(bf16, nch, bt, index, ua, G, s);
+    if (e != hipSuccess) return hip_fail(e, "up-projection launch");
+    e = cats::launch_unfused_down(bf16, nch, bt, index, ua, G, s);
+    if (e != hipSuccess) return hip_fail(e, "down-projection launch");
+    cats::ReduceArgs ra{};
+    ra.partial = ua.partial;
+    ra.G = G;
+    ra.Gseg = G;
+    ra.sum_y = 1;
+    ra.B = bp;
+    ra.d = d;
+    ra.m = m;
+    ra.residual = residual ? residual + (size_t)b0 * d : nullptr;
+    ra.y = y + (size_t)b0 * d;
+    ra.aux = 0;
+    e = cats::launch_reduce(ra, s);
+    if (e != hipSuccess) return hip_fail(e, "reduce launch");
   }
   return CATS_OK;
 }

@@ -117,11 +117,39 @@ hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 // Top-k variant: gate activations of B <= 8 rows into v [B x m], the per-row
 // cutoffs (rank r of |v| within each row) into t [B], then the fused kernel
 // reading v and t (no W_gate row).
-hipError_t launch_gate_v(int wdtype_bf16, int nch, int bt, const float* x, const void* wg, int B,
-                         int d, int m, float* v, int G, hipStream_t s);
+struct GateVArgs {
+  const void* wg;      // [m x d] W_gate^T
+  const float* x;      // [B x d]
+  int B, d, m;
+  float* v;            // [B x m] SiLU(x W_gate)
+  float t;             // with the list: the CATS threshold
+  int* seg_j;          // with the list: [m] per block, its active neurons ascending
+  uint32_t* seg_mask;  // [m] their row masks
+  int* seg_cnt;        // [G]
+};
+hipError_t launch_gate_v(int wdtype_bf16, int nch, int bt, bool seg, const GateVArgs& a, int G, hipStream_t s);
 hipError_t launch_row_select(const float* v, int B, int m, int64_t r, float* t, hipStream_t s);
 hipError_t launch_fused_bf16_topk(int nch, int bt, bool aux, const FusedArgs& a, int G, hipStream_t s);
 hipError_t launch_fused_f32_topk(int nch, int bt, bool aux, const FusedArgs& a, int G, hipStream_t s);
+
+// The MLP in separate up and down kernels (the paper's structure), rows
+// found by the mask or by the gate pass's per-block index lists.
+struct UnfusedArgs {
+  const void* wu;       // [m x d] W_up^T
+  const void* wd;       // [m x d] W_down
+  const float* x;       // [B x d]
+  const float* v;       // [B x m] gate activations
+  float t;
+  int B, d, m;
+  const int* seg_j;     // index mode: per-block active lists (gate pass)
+  const int* seg_cnt;   // [G]
+  float* h;             // [B x m] v * (x W_up): at j (mask) or at the list position (index)
+  float* partial;       // [G x B x d]
+};
+hipError_t launch_unfused_up(int wdtype_bf16, int nch, int bt, bool index, const UnfusedArgs& a, int G,
+                             hipStream_t s);
+hipError_t launch_unfused_down(int wdtype_bf16, int nch, int bt, bool index, const UnfusedArgs& a, int G,
+                               hipStream_t s);
 
 // k-steps of the batched gate/up kernel for width d (0: no instantiation
 // covers d exactly; those widths use the fused kernel).

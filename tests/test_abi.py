@@ -271,6 +271,27 @@ def test_topk_validation():
     assert call(ws=0) == WORKSPACE and call(ws_bytes=need - 1) == WORKSPACE
 
 
+def test_unfused_validation():
+    L = P.raw()
+    f = ctypes.c_float
+    need = L.cats_unfused_workspace_bytes(64, 96, 2)
+    assert need >= P.workspace_bytes(64, 96, 2, 0) + 2 * 2 * 96 * 4
+    assert L.cats_unfused_workspace_bytes(64, 96, 0) == 0 and L.cats_unfused_workspace_bytes(6, 96, 1) == 0
+
+    def call(x=A + 65536, B=2, t=0.5, mode=P.CATS_UNFUSED_MASK, res=None, y=A * 2, ws=A * 4, ws_bytes=need):
+        return L.cats_mlp_forward_unfused(ctypes.byref(_layer()), ctypes.c_void_p(x) if x else None, B, f(t), mode,
+                                          ctypes.c_void_p(res) if res else None, ctypes.c_void_p(y) if y else None,
+                                          ctypes.c_void_p(ws) if ws else None, ws_bytes, None)
+
+    assert call(x=0) == NULL and call(y=0) == NULL
+    assert call(B=0) == SHAPE and call(B=17) == SHAPE
+    assert call(mode=2) == RANGE and call(mode=-1) == RANGE
+    assert call(t=-1.0) == RANGE and call(t=math.nan) == RANGE
+    assert call(x=A + 4) == ALIGN and call(y=A + 8) == ALIGN and call(res=A + 4) == ALIGN
+    assert call(ws=0) == WORKSPACE and call(ws_bytes=need - 1) == WORKSPACE
+    assert L.cats_unfused_workspace_bytes(64, 96, 2) == need
+
+
 def test_forward_workspace_is_workspace_bytes():
     """The forward accepts exactly cats_workspace_bytes(d, m, B, 0) and up."""
     for B in (1, 3, 8, 16):
