@@ -221,11 +221,20 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_mlp_fused(FusedArgs 
     load_row(ucur, ru, row_base(mask != 0u, n0 + w + i * W));
     if (i >= 1 && i - 1 < ni) {
       const int loc = w + (i - 1) * W;
-      // The dot runs even for a masked neuron (its up row read as zeros):
-      // every buffer is then consumed on every path, which keeps the
-      // compiler's count of loads in flight exact across the loop.
+      // Every up buffer is consumed on every path, a masked neuron's too
+      // (its row reads as zeros), which keeps the compiler's count of loads
+      // in flight exact across the loop.  With several rows the dot runs on
+      // the zeros; with one row (the mask is then wave-uniform) a masked
+      // neuron only waits for its dataless load and skips the dot.
       float h[BT], u[BT];
-      row_dot(uprev, u);
+      if (BT == 1 && uniform_u32(pmask) == 0u) {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) asm volatile("" ::"v"(uprev[c]));
+#pragma unroll
+        for (int b = 0; b < BT; ++b) u[b] = 0.f;
+      } else {
+        row_dot(uprev, u);
+      }
 #pragma unroll
       for (int b = 0; b < BT; ++b) h[b] = ((pmask >> b) & 1u) ? pv[b] * u[b] : 0.f;
       if (lane == 0) {
