@@ -12,14 +12,19 @@
 namespace cats {
 
 // Batched path (bf16 weights, kBatchedMinRows..16 rows): gate and up on
-// the matrix cores, then the down-projection by column tiles.  Below 8 rows
+// the matrix cores, then the down-projection by column tiles.  Below 5 rows
 // the fused kernel is faster (one pass of its vector-ALU dot products over
-// the staged rows); above 8 it would need a second pass over the weights.
+// the staged rows); from 5 rows its dot products cost more than the
+// matrix-core path, and above 8 it would need a second pass over the weights.
 #ifndef CATS_BATCHED_MIN_ROWS
-#define CATS_BATCHED_MIN_ROWS 8
+#define CATS_BATCHED_MIN_ROWS 5
 #endif
 constexpr int kBatchedMinRows = CATS_BATCHED_MIN_ROWS;
-constexpr int kBatchedWaves = 8;
+constexpr int kBatchedWaves = 8;   // the down-projection kernel's waves per block
+// Waves of the gate/up kernel: each holds 1/16 of x's columns as matrix-core
+// operands, so at d = 4096 the operands and a tile of weights in flight fit
+// the 128 registers a wave has at four waves per SIMD.
+constexpr int kGateUpWaves = 16;
 constexpr int kDownCols = kBatchedWaves * 128;  // columns of a down-projection block
 constexpr int kDownRowChunk = 1024;             // rows a down block stages in LDS at once
 

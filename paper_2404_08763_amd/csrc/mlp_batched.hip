@@ -1,4 +1,4 @@
-// Batched CATS MLP for 8..16 rows with bf16 weights: the gate and up
+// Batched CATS MLP for 5..16 rows with bf16 weights: the gate and up
 // projections are dense contractions [B x d] . [d x m] and run on the matrix
 // cores; the down-projection is split by column tiles so that few partial
 // sums of y are written.
@@ -12,7 +12,7 @@
 // one mask, batch 1).
 //
 // Kernel 1 (k_mlp_gateup_mfma): a block owns a contiguous neuron range in
-// tiles of 16 neurons.  Each of its 8 waves owns one eighth of the columns
+// tiles of 16 neurons.  Each of its 16 waves owns one sixteenth of the columns
 // of d and keeps its slice of x in registers as the B operand of
 // v_mfma_f32_16x16x32_bf16 (x = hi + lo, both bf16: the two products carry
 // 16 bits of x's 24-bit mantissa, relative error below 2^-16 per term, with
@@ -36,6 +36,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kBW = kBatchedWaves;
 constexpr int kBThreads = kBW * kWaveSize;
+constexpr int kGW = kGateUpWaves;
+constexpr int kGThreads = kGW * kWaveSize;
 constexpr int kBTileN = 16;  // neurons per MFMA tile (and batch columns)
 
 // bf16 bit pattern nearest to f (ties to even); NaN stays a quiet NaN.
@@ -67,18 +69,18 @@ __device__ __forceinline__ void split8(const u32x4& a, const u32x4& b, bf16x8& h
 }
 
 // KS: MFMA k-steps (32 columns each) per wave; the kernel covers
-// d = kBW * 32 * KS columns exactly, so no column needs a bounds check.
+// d = kGW * 32 * KS columns exactly, so no column needs a bounds check.
 template <int KS, bool DENSE, bool AUX>
-__global__ __launch_bounds__(kBThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
+__global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
   constexpr int KW = 32 * KS;  // columns per wave
   constexpr int NBMAX = kFusedMaxNeurons;
 
-  __shared__ f32x4 red[kBW * kWaveSize];        // the waves' partial tiles
+  __shared__ f32x4 red[kGW * kWaveSize];        // the waves' partial tiles
   __shared__ float l_v[NBMAX][kBTileN];         // v of each local neuron and row
   __shared__ float l_h[NBMAX][kBTileN];         // h (0 where the row masks it)
   __shared__ uint32_t l_mask[NBMAX];            // bit b: row b keeps the neuron
-  __shared__ int w_cnt[kBW + 1];
-  __shared__ float l_ss[kBW][kBTileN];          // the waves' sums of squares per row
+  __shared__ int w_cnt[kGW + 1];
+  __shared__ float l_ss[kGW][kBTileN];          // the waves' sums of squares per row
   __shared__ float l_scale[kBTileN];            // per-row factor on every dot product
 
   const int tid = threadIdx.x;
@@ -97,7 +99,7 @@ __global__ __launch_bounds__(kBThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
   const __amdgpu_buffer_rsrc_t rg = make_rsrc(a.wg, mat_bytes);
   const __amdgpu_buffer_rsrc_t ru = make_rsrc(a.wu, mat_bytes);
 
-  for (int i = tid; i < nb; i += kBThreads) l_mask[i] = 0u;
+  for (int i = tid; i < nb; i += kGThreads) l_mask[i] = 0u;
 
   // This lane's operand coordinates: A row (neuron in tile) = lane % 16,
   // B column (batch row) = lane % 16, and 8 consecutive k at 8 * (lane / 16)
@@ -120,21 +122,13 @@ __global__ __launch_bounds__(kBThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
     return ok ? (uint32_t)(n0 + i) * row_bytes : kOOB;
   };
 
-  // the first gate tile's weights go out first: they do not depend on x
-  u32x4 buf[KS];
-  {
-    const uint32_t rb = row_of(0);
-#pragma unroll
-    for (int s = 0; s < KS; ++s) buf[s] = ld_buf16_stream(rg, rb + colb + s * 64u);
-  }
-
   // ---- x slice of this wave as hi/lo bf16 fragments (rows past B are
   // zero), loaded through a window of XWIN steps so that only the window's
   // fp32 values are live next to the fragments
   bf16x8 xh[KS], xl[KS];
   float ss = 0.f;  // sum of squares of this lane's x values (row r16)
   {
-    constexpr int XWIN = KS < 4 ? KS : 4;
+    constexpr int XWIN = KS < 8 ? KS : 8;
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, (uint32_t)(B * d * sizeof(float)));
     const uint32_t xrow = r16 < B ? (uint32_t)(r16 * d + cw0) * 4u : kOOB;
     u32x4 wa[XWIN], wb[XWIN];
@@ -165,11 +159,20 @@ __global__ __launch_bounds__(kBThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
     if (tid < kBTileN) {
       float tot = 0.f;
 #pragma unroll
-      for (int ww = 0; ww < kBW; ++ww) tot += l_ss[ww][tid];
+      for (int ww = 0; ww < kGW; ++ww) tot += l_ss[ww][tid];
       l_scale[tid] = 1.f / sqrtf(tot / (float)d + a.eps);
     }
   } else if (tid < kBTileN) {
     l_scale[tid] = 1.f;
+  }
+  // The first gate tile's weights go out only now: issued before the x
+  // fragments are built, they would sit in registers the fragments need,
+  // and the compiler parks them elsewhere one load round trip at a time.
+  u32x4 buf[KS];
+  {
+    const uint32_t rb = row_of(0);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) buf[s] = ld_buf16_stream(rg, rb + colb + s * 64u);
   }
   __syncthreads();
 
@@ -207,7 +210,7 @@ __global__ __launch_bounds__(kBThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
       const int src = jb + 16 * (i >> 2), reg = i & 3;
       float sum = 0.f;
 #pragma unroll
-      for (int ww = 0; ww < kBW; ++ww) sum += red[ww * kWaveSize + src][reg];
+      for (int ww = 0; ww < kGW; ++ww) sum += red[ww * kWaveSize + src][reg];
       sum *= l_scale[jb];
       const bool up = op >= T;
       const int li = (up ? op - T : op) * kBTileN + i;
@@ -231,20 +234,20 @@ __global__ __launch_bounds__(kBThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
 
   // ---- ordered compaction of the block's union-active neurons
   int base = 0;
-  for (int p = 0; p * kBThreads < nb; ++p) {
-    const int loc = p * kBThreads + tid;
+  for (int p = 0; p * kGThreads < nb; ++p) {
+    const int loc = p * kGThreads + tid;
     const uint32_t mk = loc < nb ? l_mask[loc] : 0u;
     const uint64_t bal = __ballot(mk != 0u);
     if (lane == 0) w_cnt[w] = __popcll(bal);
     __syncthreads();
     if (tid == 0) {
       int run = 0;
-      for (int k = 0; k < kBW; ++k) {
+      for (int k = 0; k < kGW; ++k) {
         const int c = w_cnt[k];
         w_cnt[k] = run;
         run += c;
       }
-      w_cnt[kBW] = run;
+      w_cnt[kGW] = run;
     }
     __syncthreads();
     if (mk) {
@@ -257,7 +260,7 @@ __global__ __launch_bounds__(kBThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
         if constexpr (AUX) a.seg_v[(size_t)b * m + o] = l_v[loc][b];
       }
     }
-    base += w_cnt[kBW];
+    base += w_cnt[kGW];
     __syncthreads();
   }
   if (tid == 0) a.seg_cnt[blk] = base;
@@ -389,7 +392,7 @@ __global__ __launch_bounds__(kBThreads) void k_mlp_down_cols(DownArgs a) {
 
 template <bool DENSE, bool AUX>
 static hipError_t launch_gateup_t(int ks, const BatchedArgs& a, int G, hipStream_t s) {
-  const dim3 grid(G), block(kBThreads);
+  const dim3 grid(G), block(kGThreads);
   KernelTimer timer(DENSE ? "mlp_gateup_dense" : "mlp_gateup_cats", s);
   switch (ks) {
 #define CATS_KS(K)                                                                                   \
@@ -400,9 +403,8 @@ static hipError_t launch_gateup_t(int ks, const BatchedArgs& a, int G, hipStream
     CATS_KS(1)
     CATS_KS(2)
     CATS_KS(4)
+    CATS_KS(6)
     CATS_KS(8)
-    CATS_KS(12)
-    CATS_KS(16)
 #undef CATS_KS
     default: return hipErrorInvalidValue;
   }
@@ -410,10 +412,10 @@ static hipError_t launch_gateup_t(int ks, const BatchedArgs& a, int G, hipStream
 }
 
 int batched_ks(int d) {
-  if (d % (kBW * 32) != 0) return 0;
-  const int ks = d / (kBW * 32);
+  if (d % (kGW * 32) != 0) return 0;
+  const int ks = d / (kGW * 32);
   // instantiated widths; wider rows do not fit the register-resident x slice
-  return (ks == 1 || ks == 2 || ks == 4 || ks == 8 || ks == 12 || ks == 16) ? ks : 0;
+  return (ks == 1 || ks == 2 || ks == 4 || ks == 6 || ks == 8) ? ks : 0;
 }
 
 hipError_t launch_gateup(bool dense, bool aux, const BatchedArgs& a, int G, hipStream_t s) {

@@ -72,7 +72,7 @@ def small(dev):
 
 @pytest.fixture(scope="module")
 def small_mfma(dev):
-    """d = 1024: from 8 rows on, bf16 blocks of this width take the
+    """d = 1024: from 5 rows on, bf16 blocks of this width take the
     matrix-core path, whose RMSNorm is applied inside its gate/up kernel."""
     return _small_stack(1024)
 
@@ -103,7 +103,7 @@ def test_small_stack_teacher_forced(small, oracle32, B):
           f"end-to-end drift {drift:.2e} of ||x_L - x_0||")
 
 
-@pytest.mark.parametrize("B", [8, 16])
+@pytest.mark.parametrize("B", [5, 16])
 def test_small_stack_teacher_forced_mfma(small_mfma, oracle32, B):
     layers, hws = small_mfma
     x0 = _x0(B, 1024, seed=14)
