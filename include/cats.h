@@ -60,7 +60,7 @@ typedef enum {
   CATS_ERR_ALIGN = 5,         /* a pointer misses its required alignment */
   CATS_ERR_WORKSPACE = 6,     /* workspace NULL or too small */
   CATS_ERR_HIP = 7,           /* a HIP runtime call failed */
-  CATS_ERR_UNIMPLEMENTED = 8  /* combination not supported by this build */
+  CATS_ERR_UNIMPLEMENTED = 8  /* combination the library does not implement */
 } cats_status;
 
 typedef enum { CATS_F32 = 0, CATS_BF16 = 1 } cats_dtype;

@@ -30,7 +30,7 @@
 extern "C" {
 #endif
 
-/* Name of the accumulation type of this build: "f32" or "f64". */
+/* Name of the accumulation type this copy was compiled with: "f32" or "f64". */
 const char* oracle_precision(void);
 
 /* SiLU(z) = z / (1 + exp(-z)) (Eq. 2), evaluated in the build's precision. */
