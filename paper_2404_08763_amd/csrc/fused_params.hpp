@@ -16,6 +16,11 @@ namespace cats {
 #define CATS_FUSED_BLOCKS 256
 #endif
 constexpr int kFusedWaves = CATS_FUSED_WAVES;
+// Waves of a fused-kernel block for rows of nch 16-byte chunks per lane: at
+// 16 chunks (bf16 rows of up to 8192) a wave's four row buffers alone need
+// 256 registers, so the block runs four waves, one per SIMD, which leaves
+// each wave the whole register file of its SIMD.
+constexpr int fused_waves(int nch) { return nch >= 16 ? 4 : kFusedWaves; }
 constexpr int kFusedBlocks = CATS_FUSED_BLOCKS;
 // Neurons a fused-kernel block may own (its LDS lists are this long); with
 // kFusedBlocks blocks this bounds m.
