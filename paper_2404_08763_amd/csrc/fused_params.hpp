@@ -16,11 +16,15 @@ namespace cats {
 #define CATS_FUSED_BLOCKS 256
 #endif
 constexpr int kFusedWaves = CATS_FUSED_WAVES;
-// Waves of a fused-kernel block for rows of nch 16-byte chunks per lane: at
-// 16 chunks (bf16 rows of up to 8192) a wave's four row buffers alone need
-// 256 registers, so the block runs four waves, one per SIMD, which leaves
-// each wave the whole register file of its SIMD.
-constexpr int fused_waves(int nch) { return nch >= 16 ? 4 : kFusedWaves; }
+// Waves of a fused-kernel block for rows of nch 16-byte chunks per lane and
+// a tile of bt batch rows.  One wave per SIMD when there is one row (each
+// wave then walks twice the neurons, so the per-block imbalance of the last
+// wave is half a neuron's share smaller) and at 16 chunks (bf16 rows of up
+// to 8192, whose four row buffers alone need 256 registers: a wave gets the
+// whole register file of its SIMD); two per SIMD otherwise, where the dot
+// products over several staged rows need a second wave to hide their
+// LDS reads.
+constexpr int fused_waves(int nch, int bt) { return (bt == 1 || nch >= 16) ? 4 : kFusedWaves; }
 constexpr int kFusedBlocks = CATS_FUSED_BLOCKS;
 // Neurons a fused-kernel block may own (its LDS lists are this long); with
 // kFusedBlocks blocks this bounds m.
