@@ -196,7 +196,7 @@ cats_status run_mlp(const cats_layer* L, const float* x, int32_t B, float t, boo
     da.G = G;
     da.NG = down_ng(d, m);
     da.CT = down_ct(d);
-    e = cats::launch_down_cols(da, s);
+    e = cats::launch_down_mfma(da, s);
     if (e != hipSuccess) return hip_fail(e, "down-projection launch");
     cats::ReduceArgs ra;
     ra.partial = da.partial;

@@ -160,7 +160,7 @@ hipError_t launch_unfused_down(int wdtype_bf16, int nch, int bt, bool index, con
 // covers d exactly; those widths use the fused kernel).
 int batched_ks(int d);
 hipError_t launch_gateup(bool dense, bool aux, const BatchedArgs& a, int G, hipStream_t s);
-hipError_t launch_down_cols(const DownArgs& a, hipStream_t s);
+hipError_t launch_down_mfma(const DownArgs& a, hipStream_t s);
 hipError_t launch_sparse_input(const SparseInputArgs& a, hipStream_t s);
 
 hipError_t launch_calib_acts(int wdtype_bf16, const float* x, const void* wg_t, int N, int d,

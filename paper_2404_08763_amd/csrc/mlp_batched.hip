@@ -23,10 +23,10 @@
 // ascending order with their row masks and h (the segment lists the
 // finalize step of k_mlp_reduce turns into per-row active lists).
 //
-// Kernel 2 (k_mlp_down_cols): block (column tile, neuron group) accumulates
-// h_b W_down[j, cols] over the group's union-active rows, four rows per
-// wave load (a quad of lanes per column chunk), and writes one partial y per
-// neuron group; k_mlp_reduce sums the groups in order.
+// Kernel 2 (k_mlp_down_mfma): block (column tile, neuron group) accumulates
+// h_b W_down[j, cols] over the group's union-active rows on the matrix
+// cores and writes one partial y per neuron group; k_mlp_reduce sums the
+// groups in order.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -266,17 +266,28 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
   if (tid == 0) a.seg_cnt[blk] = base;
 }
 
-// Down-projection by column tiles.  Block (ct, q): columns
-// [ct * kDownCols, +kDownCols), rows = the union-active neurons of K1 blocks
-// [q G / NG, (q+1) G / NG) in ascending order.  Wave w owns 128 columns:
-// lane = 4 * chunk + r, chunk = 8 columns, r = one of four rows loaded
-// together; the quad's four row sums are added at the end (fixed order).
-template <int BT>
-__global__ __launch_bounds__(kBThreads) void k_mlp_down_cols(DownArgs a) {
-  constexpr int RCH = kDownRowChunk;  // rows staged in LDS at a time
-  constexpr int PD = 4;               // row quads in flight per lane
-  __shared__ int s_j[RCH];
-  __shared__ __attribute__((aligned(16))) float s_h[RCH][BT];
+// Down-projection on the matrix cores (5..16 rows).  Block (ct, q) owns
+// columns [ct * kDownCols, +kDownCols) and the union-active rows of neuron
+// group q; wave w owns 128 of the columns, eight MFMA tiles of 16.  The contraction runs over neurons:
+//   D[c][b] += sum_k W_down[j_k][c] * h[b][j_k]
+// with A[c][k] = W_down[j_k][c] (16 columns x 32 rows) and B[k][b] = h[b][j_k]
+// (32 rows x 16 batch rows).  A lane's A operand is eight rows of one column,
+// which W_down's row-major layout does not hold contiguously, so each wave
+// streams its 32-row x 128-column slice of a step into its own LDS region
+// (one 256-byte run per row) and reads the operand back column-wise, two
+// bytes at a time.  h enters as bf16 hi + lo (as x does in the gate/up
+// kernel: 16 of its 24 mantissa bits, products exact, fp32 accumulation),
+// staged per block as [batch row][staged row].
+constexpr int kDmRows = 32;                 // rows per k-step
+constexpr int kDmChunk = 256;               // rows staged per block at a time
+constexpr int kDmPitch = 128 * 2 + 8;       // LDS bytes per row of a wave's slice (8 pad: q groups 16 banks apart)
+constexpr int kDmHPitch = kDmChunk + 8;     // bf16 elements per batch row of the staged h
+
+__global__ __launch_bounds__(kBThreads) void k_mlp_down_mfma(DownArgs a) {
+  __shared__ __attribute__((aligned(16))) int s_j[kDmChunk];
+  __shared__ __attribute__((aligned(16))) uint16_t s_hh[kBTileN * kDmHPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t s_hl[kBTileN * kDmHPitch];
+  __shared__ __attribute__((aligned(16))) uint8_t s_w[kBW * kDmRows * kDmPitch];
   __shared__ int s_pre[kFusedBlocks + 1];
 
   const int tid = threadIdx.x;
@@ -285,13 +296,21 @@ __global__ __launch_bounds__(kBThreads) void k_mlp_down_cols(DownArgs a) {
   const int B = a.B, d = a.d, m = a.m, G = a.G, NG = a.NG;
   const int ct = blockIdx.x % a.CT, q = blockIdx.x / a.CT;
   const int g0 = (int)(((int64_t)q * G) / NG), g1 = (int)(((int64_t)(q + 1) * G) / NG);
-  const int r = lane & 3, chunk = lane >> 2;
-  const int col = ct * kDownCols + w * 128 + chunk * 8;
-  const uint32_t colb = col < d ? (uint32_t)col * 2u : kOOB;
+  const int col0 = ct * kDownCols + w * 128;  // this wave's first column
   const uint32_t row_bytes = (uint32_t)d * 2u;
   const __amdgpu_buffer_rsrc_t rd = make_rsrc(a.wd, (uint32_t)((uint64_t)m * row_bytes));
+  uint8_t* wreg = s_w + (size_t)w * kDmRows * kDmPitch;
+  const __amdgpu_buffer_rsrc_t rh = make_rsrc(a.seg_h, (uint32_t)((size_t)B * m * sizeof(float)));
 
-  // row offsets of the group's K1 blocks
+  // streaming a step: load p (0..7) covers rows 4p + lane / 16, 16 bytes
+  // (8 columns) per lane, one 256-byte run per row
+  const int lr = lane >> 4, lc = lane & 15;
+  const int lcol = col0 + lc * 8;
+  const uint32_t lcolb = lcol < d ? (uint32_t)lcol * 2u : kOOB;
+  // operands: A lane = column i + 16 kq, B lane = batch row jb + 16 kq;
+  // both hold the eight rows 8 kq .. 8 kq + 7 of the step
+  const int oi = lane & 15, kq = lane >> 4;
+
   if (tid == 0) {
     int run = 0;
     for (int g = g0; g < g1; ++g) {
@@ -303,91 +322,127 @@ __global__ __launch_bounds__(kBThreads) void k_mlp_down_cols(DownArgs a) {
   __syncthreads();
   const int R = s_pre[g1 - g0];
 
-  float acc[BT][8];
+  f32x4 acch[8], accl[8];
 #pragma unroll
-  for (int b = 0; b < BT; ++b)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[b][e] = 0.f;
+  for (int t = 0; t < 8; ++t) {
+    acch[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    accl[t] = acch[t];
+  }
 
-  for (int c0 = 0; c0 < R; c0 += RCH) {
-    const int nr = min(RCH, R - c0);
-    for (int e = tid; e < nr; e += kBThreads) {
-      // row c0 + e lives in the segment of the K1 block whose range holds it
-      const int re = c0 + e;
-      int gi = 0;
-      while (s_pre[gi + 1] <= re) ++gi;
-      const size_t o = (size_t)(((int64_t)(g0 + gi) * m) / G) + (re - s_pre[gi]);
-      s_j[e] = a.seg_j[o];
+  for (int c0 = 0; c0 < R; c0 += kDmChunk) {
+    const int nr = min(kDmChunk, R - c0);
+    const int nsteps = (nr + kDmRows - 1) / kDmRows;
+    // stage the chunk's rows: index, and h as bf16 hi / lo by batch row
+    // (rows past nr and batch rows past B are zero).  A row's sixteen h
+    // loads are unconditional buffer loads (out of range where absent), so
+    // they are all in flight at once.
+    for (int e = tid; e < nsteps * kDmRows; e += kBThreads) {
+      int jrow = -1;
+      uint32_t o = 0;
+      if (e < nr) {
+        const int re = c0 + e;
+        int gi = 0;
+        while (s_pre[gi + 1] <= re) ++gi;
+        o = (uint32_t)(((int64_t)(g0 + gi) * m) / G) + (uint32_t)(re - s_pre[gi]);
+        jrow = a.seg_j[o];
+      }
+      s_j[e] = jrow;
+      uint32_t hb[kBTileN];
 #pragma unroll
-      for (int b = 0; b < BT; ++b) s_h[e][b] = b < B ? a.seg_h[(size_t)b * m + o] : 0.f;
+      for (int b = 0; b < kBTileN; ++b)
+        hb[b] = __builtin_amdgcn_raw_buffer_load_b32(rh, (jrow >= 0 && b < B) ? ((uint32_t)b * m + o) * 4u : kOOB, 0, 0);
+#pragma unroll
+      for (int b = 0; b < kBTileN; ++b) {
+        const float h = __uint_as_float(hb[b]);
+        const uint32_t hi = bf16_bits(h);
+        const uint32_t lo = bf16_bits(h - __uint_as_float(hi << 16));
+        s_hh[b * kDmHPitch + e] = (uint16_t)hi;
+        s_hl[b * kDmHPitch + e] = (uint16_t)lo;
+      }
     }
     __syncthreads();
-    const int nq = (nr + 3) >> 2;  // row quads
-    auto ld = [&](int qd) -> u32x4 {
-      const int e = qd * 4 + r;
-      return ld_buf16_stream(rd, (qd < nq && e < nr) ? (uint32_t)s_j[e] * row_bytes + colb : kOOB);
+
+    // a lane's rows of a step are 8 lr .. 8 lr + 7 (load p takes row
+    // 8 lr + p), so their indices come from LDS in two 16-byte reads
+    auto load_step = [&](u32x4(&buf)[8], int st) {
+      int jr[8];
+      if (st < nsteps) {
+        const int4 ja = *reinterpret_cast<const int4*>(s_j + st * kDmRows + 8 * lr);
+        const int4 jb = *reinterpret_cast<const int4*>(s_j + st * kDmRows + 8 * lr + 4);
+        jr[0] = ja.x; jr[1] = ja.y; jr[2] = ja.z; jr[3] = ja.w;
+        jr[4] = jb.x; jr[5] = jb.y; jr[6] = jb.z; jr[7] = jb.w;
+      } else {
+#pragma unroll
+        for (int p = 0; p < 8; ++p) jr[p] = -1;
+      }
+#pragma unroll
+      for (int p = 0; p < 8; ++p)
+        buf[p] = ld_buf16_stream(rd, jr[p] >= 0 ? (uint32_t)jr[p] * row_bytes + lcolb : kOOB);
     };
-    auto fma_row = [&](const u32x4& v, int qd) {
-      const int e = qd * 4 + r;
-      if (qd < nq && e < nr) {
-        float wf[8];
-        widen<wbf16>(v, wf);
-        float hv[BT];
+    // this wave's slice of a step into its LDS region (the previous step's
+    // reads by this wave come first: LDS operations of a wave run in order)
+    auto write_step = [&](const u32x4(&buf)[8]) {
 #pragma unroll
-        for (int b4 = 0; b4 < BT; b4 += 4) {
-          const f32x4 h4 = *reinterpret_cast<const f32x4*>(&s_h[e][b4]);
-          hv[b4] = h4.x;
-          hv[b4 + 1] = h4.y;
-          hv[b4 + 2] = h4.z;
-          hv[b4 + 3] = h4.w;
-        }
-#pragma unroll
-        for (int b = 0; b < BT; ++b)
-#pragma unroll
-          for (int k = 0; k < 8; ++k) acc[b][k] = fmaf(hv[b], wf[k], acc[b][k]);
+      for (int p = 0; p < 8; ++p) {
+        uint8_t* dst = wreg + (8 * lr + p) * kDmPitch + lc * 16;
+        reinterpret_cast<uint2*>(dst)[0] = uint2{buf[p].x, buf[p].y};
+        reinterpret_cast<uint2*>(dst)[1] = uint2{buf[p].z, buf[p].w};
       }
     };
-    u32x4 pb[PD];
+    auto compute_step = [&](int st) {
+      const int e0 = st * kDmRows + 8 * kq;
+      const u32x4 bh = *reinterpret_cast<const u32x4*>(s_hh + oi * kDmHPitch + e0);
+      const u32x4 bl = *reinterpret_cast<const u32x4*>(s_hl + oi * kDmHPitch + e0);
+      const bf16x8 bhv = as_bf16x8(bh), blv = as_bf16x8(bl);
 #pragma unroll
-    for (int p = 0; p < PD; ++p) pb[p] = ld(p);
-    for (int qd = 0; qd < nq; qd += PD) {
+      for (int t = 0; t < 8; ++t) {
+        const uint8_t* src = wreg + (8 * kq) * kDmPitch + (t * 16 + oi) * 2;
+        uint32_t pk[4];
 #pragma unroll
-      for (int p = 0; p < PD; ++p) {
-        const u32x4 v = pb[p];
-        pb[p] = ld(qd + p + PD);
-        fma_row(v, qd + p);
-        // one row quad at a time: its h values and products are not hoisted
-        // next to the next quad's
-        __builtin_amdgcn_sched_barrier(0);
+        for (int e2 = 0; e2 < 4; ++e2) {
+          const uint32_t lo16 = *reinterpret_cast<const uint16_t*>(src + (2 * e2) * kDmPitch);
+          const uint32_t hi16 = *reinterpret_cast<const uint16_t*>(src + (2 * e2 + 1) * kDmPitch);
+          pk[e2] = lo16 | (hi16 << 16);
+        }
+        const bf16x8 av = as_bf16x8(u32x4{pk[0], pk[1], pk[2], pk[3]});
+        acch[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bhv, acch[t], 0, 0, 0);
+        accl[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, blv, accl[t], 0, 0, 0);
+      }
+    };
+    u32x4 rA[8], rB[8];
+    load_step(rA, 0);
+    load_step(rB, 1);
+    for (int st = 0; st < nsteps; st += 2) {
+      write_step(rA);
+      load_step(rA, st + 2);
+      compute_step(st);
+      if (st + 1 < nsteps) {
+        write_step(rB);
+        load_step(rB, st + 3);
+        compute_step(st + 1);
       }
     }
-    __syncthreads();  // s_j / s_h are rewritten by the next chunk
+    __syncthreads();  // s_j / s_hh / s_hl are rewritten by the next chunk
   }
 
-  // sum the quad's four rows (lanes 4 chunk + 0..3), then lane r == 0
-  // writes this group's partial y for its 8 columns
-  float* part = a.partial + (size_t)q * B * d;
+  // D[i][j] sits in lane j + 16 (i / 4), register i % 4: batch row
+  // jb = lane % 16, columns 4 (lane / 16) .. + 3 of each tile
+  const int jb = lane & 15, c4 = (lane >> 4) * 4;
+  if (jb < B) {
+    float* part = a.partial + ((size_t)q * B + jb) * d;
 #pragma unroll
-  for (int b = 0; b < BT; ++b) {
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      float v = acc[b][k];
-      v += dpp_f32<0xb1>(v);  // quad_perm [1,0,3,2]
-      v += dpp_f32<0x4e>(v);  // quad_perm [2,3,0,1]
-      acc[b][k] = v;
+    for (int t = 0; t < 8; ++t) {
+      const int c = col0 + t * 16 + c4;
+      if (c < d) *reinterpret_cast<f32x4*>(part + c) = acch[t] + accl[t];
     }
   }
-  if (r == 0 && col < d) {
-#pragma unroll
-    for (int b = 0; b < BT; ++b) {
-      if (b < B) {
-        f32x4 o0 = {acc[b][0], acc[b][1], acc[b][2], acc[b][3]};
-        f32x4 o1 = {acc[b][4], acc[b][5], acc[b][6], acc[b][7]};
-        *reinterpret_cast<f32x4*>(part + (size_t)b * d + col) = o0;
-        *reinterpret_cast<f32x4*>(part + (size_t)b * d + col + 4) = o1;
-      }
-    }
-  }
+}
+
+hipError_t launch_down_mfma(const DownArgs& a, hipStream_t s) {
+  const dim3 grid(a.CT * a.NG), block(kBThreads);
+  KernelTimer timer("mlp_down_mfma", s);
+  hipExtLaunchKernelGGL(k_mlp_down_mfma, grid, block, 0, s, timer.start(), timer.stop(), 0, a);
+  return hipGetLastError();
 }
 
 template <bool DENSE, bool AUX>
@@ -424,16 +479,6 @@ hipError_t launch_gateup(bool dense, bool aux, const BatchedArgs& a, int G, hipS
   return aux ? launch_gateup_t<false, true>(ks, a, G, s) : launch_gateup_t<false, false>(ks, a, G, s);
 }
 
-hipError_t launch_down_cols(const DownArgs& a, hipStream_t s) {
-  const dim3 grid(a.CT * a.NG), block(kBThreads);
-  KernelTimer timer("mlp_down_cols", s);
-  if (a.B <= 4)
-    hipExtLaunchKernelGGL(k_mlp_down_cols<4>, grid, block, 0, s, timer.start(), timer.stop(), 0, a);
-  else if (a.B <= 8)
-    hipExtLaunchKernelGGL(k_mlp_down_cols<8>, grid, block, 0, s, timer.start(), timer.stop(), 0, a);
-  else
-    hipExtLaunchKernelGGL(k_mlp_down_cols<16>, grid, block, 0, s, timer.start(), timer.stop(), 0, a);
-  return hipGetLastError();
-}
+
 
 }  // namespace cats
