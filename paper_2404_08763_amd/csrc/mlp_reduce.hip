@@ -7,7 +7,10 @@
 
 namespace cats {
 
-constexpr int kReduceThreads = 256;
+// Eight waves, eight consecutive float4 columns: a block reads whole
+// 128-byte lines of every partial row, so no line is fetched by two blocks
+// (consecutive blocks run on different XCDs, whose L2s do not share lines).
+constexpr int kReduceThreads = 512;
 constexpr int kReduceWaves = kReduceThreads / kWaveSize;    // float4 columns per block
 constexpr int kReducePer = kFusedBlocks / kWaveSize;        // partials per lane
 static_assert(kFusedBlocks % kWaveSize == 0, "partials must split evenly over the lanes");
