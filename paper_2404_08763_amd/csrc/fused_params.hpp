@@ -23,8 +23,11 @@ constexpr int kFusedWaves = CATS_FUSED_WAVES;
 // to 8192, whose four row buffers alone need 256 registers: a wave gets the
 // whole register file of its SIMD); two per SIMD otherwise, where the dot
 // products over several staged rows need a second wave to hide their
-// LDS reads.
-constexpr int fused_waves(int nch, int bt) { return (bt == 1 || nch >= 16) ? 4 : kFusedWaves; }
+// LDS reads, and when the gate activations are given (vin: no gate rows
+// stream, so a wave has fewer loads in flight and two per SIMD keep more).
+constexpr int fused_waves(int nch, int bt, bool vin) {
+  return ((bt == 1 && !vin) || nch >= 16) ? 4 : kFusedWaves;
+}
 constexpr int kFusedBlocks = CATS_FUSED_BLOCKS;
 // Neurons a fused-kernel block may own (its LDS lists are this long); with
 // kFusedBlocks blocks this bounds m.

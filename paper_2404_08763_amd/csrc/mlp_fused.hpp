@@ -43,12 +43,12 @@ namespace cats {
 // VIN: the gate activations v (and one threshold per row) come precomputed
 // (the per-token top-k variant); no W_gate row is read.
 template <typename WT, int NCH, int BT, bool DENSE, bool AUX, bool VIN>
-__global__ __launch_bounds__(fused_waves(NCH, BT)* kWaveSize) void k_mlp_fused(FusedArgs a) {
+__global__ __launch_bounds__(fused_waves(NCH, BT, VIN)* kWaveSize) void k_mlp_fused(FusedArgs a) {
   typedef typename wtraits<WT>::elem E;
   constexpr int VEC = wtraits<WT>::VEC;
   constexpr int CH = kWaveSize * VEC;  // elements per chunk
   constexpr int DP = NCH * CH;         // padded row length in LDS
-  constexpr int W = fused_waves(NCH, BT);
+  constexpr int W = fused_waves(NCH, BT, VIN);
   constexpr int NT = W * kWaveSize;
   constexpr int QMAX = (NCH + W - 1) / W;  // down-stage chunks per wave
   constexpr int RB = QMAX >= 4 ? 2 : 8 / QMAX;  // down rows per batch
@@ -390,7 +390,7 @@ __global__ __launch_bounds__(fused_waves(NCH, BT)* kWaveSize) void k_mlp_fused(F
 template <typename WT, bool DENSE, bool AUX, bool VIN, int NCH>
 hipError_t launch_fused_nch(int bt, const FusedArgs& a, int G, hipStream_t s) {
   constexpr int DP = NCH * kWaveSize * wtraits<WT>::VEC;
-  const dim3 grid(G), block(fused_waves(NCH, bt) * kWaveSize);
+  const dim3 grid(G), block(fused_waves(NCH, bt, VIN) * kWaveSize);
   KernelTimer timer(VIN ? "mlp_fused_topk" : (DENSE ? "mlp_fused_dense" : "mlp_fused_cats"), s);
   switch (bt) {
     case 1: hipExtLaunchKernelGGL((k_mlp_fused<WT, NCH, 1, DENSE, AUX, VIN>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
