@@ -124,6 +124,26 @@ def test_bf16_ragged_shapes(dev, oracle32, d, m):
             check_forward(y, aux, ref, t, 1, f"d{d} m{m} k{k} b{b}", ref_all=all0[b], w_down=hw[2])
 
 
+@pytest.mark.parametrize("dtype,d,m,B", [(torch.bfloat16, 8192, 2600, 1), (torch.bfloat16, 8192, 2600, 3),
+                                         (torch.float32, 4096, 1500, 1), (torch.float32, 4096, 1500, 2)])
+def test_wide_rows(dev, oracle32, dtype, d, m, B):
+    """Rows of 16 chunks per lane (bf16 d = 8192, fp32 d = 4096): the fused
+    kernel runs four waves per block there, each wave holding its row
+    buffers in the whole register file of a SIMD; about 10 neurons per block."""
+    c = W.shrink(W.CONFIGS["C3"], d, m)
+    wg, wu, wd = W.weights(d, m, dtype, layer=8)
+    layer = device_layer(wg, wu, wd)
+    hw = host_f32(wg, wu, wd)
+    x = W.decode_vectors(c, B)
+    ref_all = oracle32.cats_mlp(x.numpy(), *hw, t=0.0)
+    for k in (0.0, 0.6):
+        t = quantile_t(np.abs(ref_all["v"]), k) if k > 0 else 0.0
+        say("wide rows", dtype, d, m, "B", B, "k", k)
+        y, aux = P.mlp_forward(layer, x.cuda(), t, aux=True)
+        ref = ref_all if k == 0 else oracle32.cats_mlp(x.numpy(), *hw, t=t)
+        check_forward(y, aux, ref, t, B, f"wide {dtype} d{d} B{B} k{k}", ref_all=ref_all, w_down=hw[2])
+
+
 @pytest.mark.parametrize("B", [2, 3, 4, 8, 16])
 def test_batch_rows_have_their_own_masks(dev, oracle32, B):
     d, m = 1024, 1500
