@@ -33,6 +33,7 @@
 namespace cats {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short v4i16 __attribute__((ext_vector_type(4)));
 
 constexpr int kBW = kBatchedWaves;
 constexpr int kBThreads = kBW * kWaveSize;
@@ -266,18 +267,19 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
   if (tid == 0) a.seg_cnt[blk] = base;
 }
 
-// Down-projection on the matrix cores (5..16 rows).  Block (ct, q) owns
+// Down-projection on the matrix cores (5..16 rows). Block (ct, q) owns
 // columns [ct * kDownCols, +kDownCols) and the union-active rows of neuron
-// group q; wave w owns 128 of the columns, eight MFMA tiles of 16.  The contraction runs over neurons:
-//   D[c][b] += sum_k W_down[j_k][c] * h[b][j_k]
-// with A[c][k] = W_down[j_k][c] (16 columns x 32 rows) and B[k][b] = h[b][j_k]
-// (32 rows x 16 batch rows).  A lane's A operand is eight rows of one column,
-// which W_down's row-major layout does not hold contiguously, so each wave
-// streams its 32-row x 128-column slice of a step into its own LDS region
-// (one 256-byte run per row) and reads the operand back column-wise, two
-// bytes at a time.  h enters as bf16 hi + lo (as x does in the gate/up
-// kernel: 16 of its 24 mantissa bits, products exact, fp32 accumulation),
-// staged per block as [batch row][staged row].
+// group q; wave w owns 128 of the columns, eight MFMA tiles of 16. The
+// contraction runs over neurons:
+//  D[c][b] += sum_k W_down[j_k][c] * h[b][j_k]
+// with A[c][k] = W_down[j_k][c] (16 columns x 32 rows) and B[k][b] =
+// h[b][j_k] (32 rows x 16 batch rows). A lane's A operand is eight rows of
+// one column, which W_down's row-major layout does not hold contiguously, so
+// each wave streams its 32-row x 128-column slice of a step into its own LDS
+// region (one 256-byte run per row) and reads the operand back column-wise
+// with gfx950's transposing LDS reads. h enters as bf16 hi + lo (as x does in
+// the gate/up kernel: 16 of its 24 mantissa bits, products exact, fp32
+// accumulation), staged per block as [batch row][staged row].
 constexpr int kDmRows = 32;                 // rows per k-step
 constexpr int kDmChunk = 256;               // rows staged per block at a time
 constexpr int kDmPitch = 128 * 2 + 8;       // LDS bytes per row of a wave's slice (8 pad: q groups 16 banks apart)
@@ -394,17 +396,20 @@ __global__ __launch_bounds__(kBThreads) void k_mlp_down_mfma(DownArgs a) {
       const u32x4 bh = *reinterpret_cast<const u32x4*>(s_hh + oi * kDmHPitch + e0);
       const u32x4 bl = *reinterpret_cast<const u32x4*>(s_hl + oi * kDmHPitch + e0);
       const bf16x8 bhv = as_bf16x8(bh), blv = as_bf16x8(bl);
+      // A operand by transposing reads: in each 16-lane group, lane r
+      // names four consecutive 16-bit values (row 8 kq + r / 4, columns
+      // 4 (r % 4) .. + 3 of the tile) and lane i receives value i % 4 of the
+      // rows named by lanes i / 4 + 4 k, k = 0..3: column i of four
+      // consecutive rows.  Two reads give the eight rows of a step's half.
+      const int ar = 8 * kq + (oi >> 2);
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
-        const uint8_t* src = wreg + (8 * kq) * kDmPitch + (t * 16 + oi) * 2;
-        uint32_t pk[4];
-#pragma unroll
-        for (int e2 = 0; e2 < 4; ++e2) {
-          const uint32_t lo16 = *reinterpret_cast<const uint16_t*>(src + (2 * e2) * kDmPitch);
-          const uint32_t hi16 = *reinterpret_cast<const uint16_t*>(src + (2 * e2 + 1) * kDmPitch);
-          pk[e2] = lo16 | (hi16 << 16);
-        }
-        const bf16x8 av = as_bf16x8(u32x4{pk[0], pk[1], pk[2], pk[3]});
+        const uint8_t* src = wreg + ar * kDmPitch + (t * 16 + 4 * (oi & 3)) * 2;
+        const v4i16 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)src);
+        const v4i16 r1 =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(src + 4 * kDmPitch));
+        const uint2 w0 = __builtin_bit_cast(uint2, r0), w1 = __builtin_bit_cast(uint2, r1);
+        const bf16x8 av = as_bf16x8(u32x4{w0.x, w0.y, w1.x, w1.y});
         acch[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bhv, acch[t], 0, 0, 0);
         accl[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, blv, accl[t], 0, 0, 0);
       }
