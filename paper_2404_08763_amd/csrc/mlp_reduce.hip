@@ -14,6 +14,12 @@ constexpr int kReduceThreads = 512;
 constexpr int kReduceWaves = kReduceThreads / kWaveSize;    // float4 columns per block
 constexpr int kReducePer = kFusedBlocks / kWaveSize;        // partials per lane
 static_assert(kFusedBlocks % kWaveSize == 0, "partials must split evenly over the lanes");
+// List finalize: entries per thread per pass, and one count per wave and
+// entry slot, which one wave scans.
+constexpr int kFinPer = 8;
+constexpr int kFinPass = kFinPer * kReduceThreads;
+constexpr int kFinCounts = kFinPer * kReduceWaves;
+static_assert(kFinCounts == kWaveSize, "one wave scans a pass's counts");
 
 __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
   const int tid = threadIdx.x;
@@ -64,45 +70,105 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
     return;
   }
 
-  // Finalize the active lists of row b: segment g (one per fused block)
-  // starts at its block's first neuron and is ascending; segments are in
-  // neuron order, so concatenating the entries whose row bit b is set gives
-  // the ascending list.
-  __shared__ int offs[kFusedBlocks + 1];
+  // Finalize the active lists of row b.  Entry p of the segment arrays
+  // belongs to segment g(p), the last one whose start floor(g m / Gseg) is
+  // at most p, and names a union-active neuron when it is among the first
+  // seg_cnt[g] entries of its segment.  Segments are ascending and in neuron
+  // order, so row b's list is the named entries with bit b set, taken in
+  // order of p: an ordered stream compaction.  A pass covers kFinPass entries, kFinPer per thread at a
+  // stride of the block (coalesced); a ballot counts each wave's 64 entries
+  // of a pass and one wave scans the pass's 64 counts in entry order.
+  __shared__ int s_base[kFusedBlocks + 1];  // segment starts floor(g m / Gseg)
+  __shared__ int s_end[kFusedBlocks];       // ends of the segments' named entries
+  __shared__ int s_off[kFinCounts + 1];
   const int b = blockIdx.x - nred;
-  for (int g = tid; g < a.Gseg; g += kReduceThreads) {
-    const int base = (int)(((int64_t)g * a.m) / a.Gseg);
-    const int sc = a.seg_cnt[g];
-    int mine = 0;
-    for (int e = 0; e < sc; ++e) mine += (int)((a.seg_mask[base + e] >> b) & 1u);
-    offs[g] = mine;
-  }
-  __syncthreads();
-  if (tid == 0) {  // exclusive scan over the segment counts
-    int run = 0;
-    for (int k = 0; k < a.Gseg; ++k) {
-      const int c = offs[k];
-      offs[k] = run;
-      run += c;
+  const int w = tid / kWaveSize;
+  const int G = a.Gseg, m = a.m;
+  const uint32_t mb = (uint32_t)m * 4u;
+  const __amdgpu_buffer_rsrc_t rm = make_rsrc(a.seg_mask, mb);
+  const __amdgpu_buffer_rsrc_t rj = make_rsrc(a.active_idx ? a.seg_j : nullptr, a.active_idx ? mb : 0u);
+  const __amdgpu_buffer_rsrc_t rv =
+      make_rsrc(a.active_v ? a.seg_v + (size_t)b * m : nullptr, a.active_v ? mb : 0u);
+  const __amdgpu_buffer_rsrc_t rh =
+      make_rsrc(a.active_h ? a.seg_h + (size_t)b * m : nullptr, a.active_h ? mb : 0u);
+  const uint64_t below = (1ull << lane) - 1ull;
+  const float gm = (float)G / (float)m;
+  struct Pass {
+    uint32_t mk[kFinPer], jv[kFinPer], vv[kFinPer], hv[kFinPer];
+  };
+  auto load = [&](Pass& f, int p0) {  // entries past m read as zero, no traffic
+#pragma unroll
+    for (int k = 0; k < kFinPer; ++k) {
+      const int p = p0 + k * kReduceThreads + tid;
+      const uint32_t off = p < m ? (uint32_t)p * 4u : kOOB;
+      f.mk[k] = __builtin_amdgcn_raw_buffer_load_b32(rm, off, 0, 0);
+      f.jv[k] = __builtin_amdgcn_raw_buffer_load_b32(rj, off, 0, 0);
+      f.vv[k] = __builtin_amdgcn_raw_buffer_load_b32(rv, off, 0, 0);
+      f.hv[k] = __builtin_amdgcn_raw_buffer_load_b32(rh, off, 0, 0);
     }
-    offs[a.Gseg] = run;
-  }
-  __syncthreads();
-  for (int g = tid; g < a.Gseg; g += kReduceThreads) {
-    const int base = (int)(((int64_t)g * a.m) / a.Gseg);
-    const int sc = a.seg_cnt[g];
-    int pos = offs[g];
-    for (int e = 0; e < sc; ++e) {
-      if ((a.seg_mask[base + e] >> b) & 1u) {
-        const size_t o = (size_t)b * a.m + pos;
-        if (a.active_idx) a.active_idx[o] = a.seg_j[base + e];
-        if (a.active_v) a.active_v[o] = a.seg_v[(size_t)b * a.m + base + e];
-        if (a.active_h) a.active_h[o] = a.seg_h[(size_t)b * a.m + base + e];
-        ++pos;
+  };
+  int run = 0;  // list entries of row b before the current pass
+  auto compact = [&](const Pass& f, int p0) {
+    uint64_t bal[kFinPer];
+#pragma unroll
+    for (int k = 0; k < kFinPer; ++k) {
+      const int p = p0 + k * kReduceThreads + tid;
+      bool keep = false;
+      if (p < m) {
+        // g(p) from an fp32 estimate (off by at most one where segments are
+        // wider than one entry), moved to the last segment starting at or
+        // before p
+        int g = min((int)((float)p * gm), G - 1);
+        while (g + 1 < G && s_base[g + 1] <= p) ++g;
+        while (s_base[g] > p) --g;
+        keep = p < s_end[g] && ((f.mk[k] >> b) & 1u);
+      }
+      bal[k] = __ballot(keep);
+      if (lane == 0) s_off[k * kReduceWaves + w] = __popcll(bal[k]);
+    }
+    __syncthreads();
+    if (w == 0) {  // exclusive scan of the 64 counts, entry order = (k, w)
+      const int c = s_off[lane];
+      int incl = c;
+#pragma unroll
+      for (int o = 1; o < kWaveSize; o <<= 1) {
+        const int v = __shfl_up(incl, o);
+        if (lane >= o) incl += v;
+      }
+      s_off[lane] = incl - c;
+      if (lane == kWaveSize - 1) s_off[kFinCounts] = incl;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kFinPer; ++k) {
+      if ((bal[k] >> lane) & 1ull) {
+        const size_t o = (size_t)b * m + run + s_off[k * kReduceWaves + w] + __popcll(bal[k] & below);
+        if (a.active_idx) a.active_idx[o] = (int)f.jv[k];
+        if (a.active_v) a.active_v[o] = __uint_as_float(f.vv[k]);
+        if (a.active_h) a.active_h[o] = __uint_as_float(f.hv[k]);
       }
     }
+    run += s_off[kFinCounts];
+    __syncthreads();  // s_off is rewritten by the next pass
+  };
+  // The next pass's loads are in flight while a pass is compacted.
+  Pass fa, fb;
+  load(fa, 0);
+  for (int g = tid; g <= G; g += kReduceThreads) {
+    const int base = (int)(((int64_t)g * m) / G);
+    s_base[g] = base;
+    if (g < G) s_end[g] = base + a.seg_cnt[g];
   }
-  if (tid == 0 && a.active_cnt) a.active_cnt[b] = offs[a.Gseg];
+  __syncthreads();
+  for (int p0 = 0; p0 < m; p0 += 2 * kFinPass) {
+    load(fb, p0 + kFinPass);
+    compact(fa, p0);
+    if (p0 + kFinPass < m) {
+      load(fa, p0 + 2 * kFinPass);
+      compact(fb, p0 + kFinPass);
+    }
+  }
+  if (tid == 0 && a.active_cnt) a.active_cnt[b] = run;
 }
 
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s) {
