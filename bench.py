@@ -12,9 +12,11 @@ value = sum of required bytes / timed wall time, where a call's required
 bytes are s_w*d*(m + 2*n_act) + 8*d + 8*n_act with n_act the measured active
 count of that token (full W_gate, plus the active rows of W_up and W_down).
 
-Also reported: per-sparsity us and GB/s, the dense kernel, the roofline of
-the dominant kernel (HIP events on its launch stream over an identical
-timed region), the CPU oracle on a bounded sample (baseline only), and two
+Also reported: per-sparsity us and GB/s (with per-call median / geomean /
+p10 / p90, and warm figures without rotation), the dense kernel, the
+roofline of the dominant kernel (HIP events on its launch stream over an
+identical timed region) against the rated peak and against the attainable
+read bandwidth of a plain stream measured in the same run, the CPU oracle on a bounded sample (baseline only), and two
 extras: the 40-layer Llama2-13B-shaped stack at k=0.5 (us per layer over a
 128-step decode chain) and the 32-layer Llama2-7B-shaped stack at batch
 1..16 and k=0.5 / 0.7 against dense (where sparsity stops paying), and CATS on
@@ -147,7 +149,7 @@ def bench_stack_c4(P, W, torch, timed, steps, warm):
                                        round(float(1 - nact.mean(0).min() / c.m), 4)],
         "fused_kernel_avg_us": round(fused_us, 3),
         "fused_kernel_frac": round(kb / (fused_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
-        "kernel_avg_us": {n: round(v[1] * 1e3 / max(1, v[0]), 3) for n, v in kt.items()},
+        "kernel_avg_us": {n: round(v[1] * 1e3 / v[0], 3) for n, v in kt.items() if v[0]},
         "weights_gen_s": round(gen_s, 2), "calib_s": round(calib_s, 2),
         "thresholds_min_max": [round(min(ts), 5), round(max(ts), 5)],
     }
@@ -187,7 +189,7 @@ def bench_batch_c5(P, W, torch, timed, steps, warm):
         P.timer_enable(True)
         timed(lambda s: _stack_call(P, dense, xb[s % nbat], out, ws, stream), 0, 4)
         P.timer_enable(False)
-        row["dense_kernel_avg_us"] = {n: round(v[1] * 1e3 / max(1, v[0]), 3) for n, v in P.timer_read().items()}
+        row["dense_kernel_avg_us"] = {n: round(v[1] * 1e3 / v[0], 3) for n, v in P.timer_read().items() if v[0]}
         for k in c.sparsities:
             U = np.stack([_union_counts(P, stacks[k], xb[i], ws) for i in range(nbat)])  # [nbat, L]
             ms = timed(lambda s: _stack_call(P, stacks[k], xb[s % nbat], out, ws, stream), warm, steps)
@@ -211,6 +213,64 @@ def bench_batch_c5(P, W, torch, timed, steps, warm):
                                         "from_bytes": min(pred) if pred else None}
     res["thresholds_k_min_max"] = {str(k): [round(min(v), 5), round(max(v), 5)] for k, v in ts.items()}
     return res
+
+
+def bench_attainable(P, torch, dev, launch_bytes, reps=12):
+    """Attainable HBM read bandwidth: the library's plain stream with the
+    weight kernels' 16-byte non-temporal loads, best over a sweep of grid
+    size, loads in flight and access order (mean launch, HIP events on the
+    launch stream), at two sizes: 1 GiB (4x the MALL; the steady state) and
+    the dominant kernel's bytes per launch (what one launch of a plain read
+    of the same bytes takes, start and tail included).  Launches rotate over
+    distinct slices of a 1 GiB buffer so none finds its bytes cached."""
+    nbytes = 1 << 30
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device=dev).view(torch.uint8)
+    sink = torch.zeros(65536, dtype=torch.int32, device=dev)
+
+    def sweep(size):
+        n = max(1, min(8, nbytes // size))
+        sl = [buf[i * size:(i + 1) * size] for i in range(n)]
+        rows = []
+        for blocks in (256, 512, 1024, 4096):
+            for inflight in (4, 8, 16):
+                for runs in (False, True):
+                    for i in range(3):
+                        P.stream_read(sl[i % n], blocks, inflight, runs, sink)
+                    torch.cuda.synchronize()
+                    P.timer_reset()
+                    P.timer_enable(True)
+                    for i in range(reps):
+                        P.stream_read(sl[i % n], blocks, inflight, runs, sink)
+                    torch.cuda.synchronize()
+                    P.timer_enable(False)
+                    c, ms = P.timer_read()["stream_read"]
+                    rows.append((size / (ms / c * 1e-3) / 1e9, ms / c * 1e3, blocks, inflight, runs))
+        b = max(rows)
+        return {"gbps": round(b[0], 1), "us": round(b[1], 3), "bytes": size,
+                "config": {"blocks": b[2], "threads": 256, "inflight": b[3], "runs": b[4]},
+                "sweep_min_gbps": round(min(rows)[0], 1), "configs": len(rows)}
+
+    out = {"steady": sweep(nbytes), "one_launch": sweep(launch_bytes // 16 * 16)}
+    del buf, sink
+    return out
+
+
+def per_call_stats(torch, fn, n_warm, n):
+    """Per-call durations (HIP events around each call) in us."""
+    import numpy as np
+
+    for s in range(n_warm):
+        fn(s)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    torch.cuda.synchronize()
+    for s in range(n):
+        ev[s][0].record()
+        fn(n_warm + s)
+        ev[s][1].record()
+    torch.cuda.synchronize()
+    us = np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+    return {"median": round(float(np.median(us)), 3), "geomean": round(float(np.exp(np.log(us).mean())), 3),
+            "p10": round(float(np.percentile(us, 10)), 3), "p90": round(float(np.percentile(us, 90)), 3)}
 
 
 def bench_sparse_input(P, W, torch, timed, steps, warm, rotate):
@@ -519,6 +579,11 @@ def main() -> int:
         dense_us = msd * 1e3 / K
         dense_gbps = req_bytes(m) / (dense_us * 1e-6) / 1e9
         out["us_per_layer"] = {str(k): round(per_k[k][0], 3) for k in ks}
+        out["per_call_us"] = {str(k): per_call_stats(torch, lambda s, k=k: call_cats(s % R, s % ntok, k), Wm, K)
+                              for k in ks}
+        # one weight copy, no rotation: part of the weights stays in the MALL
+        out["warm_us_per_layer"] = {
+            str(k): round(timed(lambda s, k=k: call_cats(0, s % ntok, k), Wm, K) * 1e3 / K, 3) for k in ks}
         out["gbps"] = {str(k): round(per_k[k][1], 1) for k in ks}
         out["frac_of_hbm_peak"] = {str(k): round(per_k[k][1] / HBM_PEAK_GBPS, 4) for k in ks}
         out["dense_us_per_layer"] = round(dense_us, 3)
@@ -562,7 +627,14 @@ def main() -> int:
             "traffic": fused_traffic(cfg.name), "avg_launch_us": round(avg_us, 3), "launches": n_launch,
             "bytes_per_launch": int(k1_total / max(1, n_launch)),
         }
-        out["kernel_avg_us"] = {n: round(v[1] * 1e3 / max(1, v[0]), 3) for n, v in kt.items()}
+        att = bench_attainable(P, torch, dev, out["roofline"]["bytes_per_launch"])
+        out["attainable_read"] = att
+        out["roofline"]["attainable"] = att["steady"]["gbps"]
+        out["roofline"]["frac_of_attainable"] = round(achieved / att["steady"]["gbps"], 4)
+        out["roofline"]["plain_read_one_launch_us"] = att["one_launch"]["us"]
+        out["roofline"]["frac_of_plain_read_one_launch"] = round(att["one_launch"]["us"] / avg_us, 4)
+        log(f"[bench] attainable read {att}")
+        out["kernel_avg_us"] = {n: round(v[1] * 1e3 / v[0], 3) for n, v in kt.items() if v[0]}
         out["timed_region_with_kernel_events_ms_per_step"] = round(ms_timer / K, 5)
         out["topk"] = bench_topk(P, W, torch, timed, layers, xs, ks, dense_us, K, Wm)
         log(f"[bench] top-k: {out['topk']}")

@@ -280,6 +280,19 @@ cats_status cats_calibrate_stack(const cats_layer* layers, int32_t L, const floa
 cats_status cats_rmsnorm(const float* x, float* xn, int32_t B, int32_t d, float eps,
                          void* stream);
 
+/* Attainable read bandwidth (a measurement aid; nothing of the method):
+ * streams `bytes` of device memory at `buf` (16-byte aligned, a positive
+ * multiple of 16, at most 1 GiB) with the 16-byte non-temporal loads the
+ * weight kernels use, from `blocks` (1..65536) workgroups of 256 threads,
+ * each lane keeping `inflight` (4, 8 or 16) loads of a step outstanding.
+ * runs = 0: a step's loads of all waves lie side by side (wave w reads the
+ * w-th KB of each 1 KB x waves stripe); runs = 1: each wave reads its own
+ * run of `inflight` KB.  `sink` is a device u32 array of `blocks` entries
+ * that the kernel may write (contents meaningless).  Enqueue only; the
+ * launch is timed under the name "stream_read" by cats_timer_*. */
+cats_status cats_stream_read(const void* buf, size_t bytes, int32_t blocks, int32_t inflight, int32_t runs,
+                             uint32_t* sink, void* stream);
+
 /* Per-kernel timing.  While enabled, every kernel the library launches is
  * bracketed by HIP events recorded on its launch stream.  cats_timer_get
  * waits for the pending events and returns, for kernel name i, the number

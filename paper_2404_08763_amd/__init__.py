@@ -31,6 +31,7 @@ from ._lib import (  # noqa: F401
     sparse_input_workspace,
     stack_forward,
     threshold_from_acts,
+    stream_read,
     timer_enable,
     timer_read,
     timer_reset,

@@ -79,6 +79,7 @@ _SIGNATURES = {
     "cats_unfused_workspace_bytes": ([_i32, _i32, _i32], _sz),
     "cats_mlp_forward_unfused": ([ctypes.POINTER(_Layer), _vp, _i32, _f32, _i32, _vp, _vp, _vp, _sz, _vp], _i32),
     "cats_rmsnorm": ([_vp, _vp, _i32, _i32, _f32, _vp], _i32),
+    "cats_stream_read": ([_vp, _sz, _i32, _i32, _i32, _vp, _vp], _i32),
     "cats_timer_enable": ([_i32], _i32),
     "cats_timer_reset": ([], _i32),
     "cats_timer_count": ([], _i32),
@@ -484,6 +485,18 @@ def rmsnorm(x: torch.Tensor, eps: float = 1e-5, out: Optional[torch.Tensor] = No
     d = int(x.shape[-1])
     _check(raw().cats_rmsnorm(_ptr(x), _ptr(out), B, d, float(eps), _stream()))
     return out
+
+
+def stream_read(buf: torch.Tensor, blocks: int, inflight: int = 8, runs: bool = False,
+                sink: Optional[torch.Tensor] = None) -> None:
+    """Enqueue one plain read of a device tensor's bytes (attainable-bandwidth
+    probe; time it with timer_* under the name "stream_read")."""
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous device tensor")
+    if sink is None:
+        sink = torch.empty(blocks, dtype=torch.int32, device=buf.device)
+    _check(raw().cats_stream_read(_ptr(buf), buf.numel() * buf.element_size(), int(blocks), int(inflight),
+                                  1 if runs else 0, _ptr(sink), _stream()))
 
 
 def timer_enable(on: bool = True) -> None:

@@ -929,6 +929,23 @@ cats_status cats_rmsnorm(const float* x, float* xn, int32_t B, int32_t d, float 
   return CATS_OK;
 }
 
+cats_status cats_stream_read(const void* buf, size_t bytes, int32_t blocks, int32_t inflight, int32_t runs,
+                             uint32_t* sink, void* stream) {
+  if (!buf || !sink) return fail(CATS_ERR_NULL, "buf or sink is NULL");
+  if (bytes == 0 || bytes % 16 != 0 || bytes > cats::kStreamReadMaxBytes)
+    return fail(CATS_ERR_SHAPE, "bytes=%zu must be a positive multiple of 16 of at most %llu", bytes,
+                (unsigned long long)cats::kStreamReadMaxBytes);
+  if (blocks < 1 || blocks > 65536) return fail(CATS_ERR_SHAPE, "blocks=%d outside [1, 65536]", (int)blocks);
+  if (inflight != 4 && inflight != 8 && inflight != 16)
+    return fail(CATS_ERR_RANGE, "inflight=%d must be 4, 8 or 16", (int)inflight);
+  if (runs != 0 && runs != 1) return fail(CATS_ERR_RANGE, "runs=%d must be 0 or 1", (int)runs);
+  if (!aligned(buf, 16) || !aligned(sink, 4)) return fail(CATS_ERR_ALIGN, "buf must be 16-byte aligned, sink 4");
+  hipError_t e = cats::launch_stream_read(buf, (uint32_t)bytes, blocks, inflight, runs != 0, sink,
+                                          static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "stream read launch");
+  return CATS_OK;
+}
+
 cats_status cats_timer_enable(int32_t on) {
   TimerState& T = timer_state();
   std::lock_guard<std::mutex> lk(T.mu);

@@ -171,6 +171,11 @@ hipError_t launch_radix_select(const float* a, int64_t n, int64_t r, uint32_t* s
                                hipStream_t s);
 
 hipError_t launch_rmsnorm(const float* x, float* xn, int B, int d, float eps, hipStream_t s);
+constexpr uint64_t kStreamReadMaxBytes = 1ull << 30;
+// Plain read of bytes (a multiple of 16, at most kStreamReadMaxBytes) at buf by
+// blocks x 256 threads with inflight (4, 8, 16) 16-byte loads per lane.
+hipError_t launch_stream_read(const void* buf, uint32_t bytes, int blocks, int inflight, bool runs, uint32_t* sink,
+                              hipStream_t s);
 hipError_t launch_transpose(const void* in, void* out, int rows, int cols, int elem_bytes,
                             hipStream_t s);
 

@@ -314,3 +314,17 @@ def test_no_device_is_a_hip_error_not_a_crash():
     st = L.cats_rmsnorm(ctypes.c_void_p(A), ctypes.c_void_p(A * 2), 1, 64, ctypes.c_float(1e-5), None)
     assert st == HIP
     assert L.cats_last_error()
+
+
+def test_stream_read_validation():
+    L = P.raw()
+
+    def call(buf=A, nbytes=1 << 20, blocks=1024, inflight=8, runs=0, sink=A * 2):
+        return L.cats_stream_read(ctypes.c_void_p(buf) if buf else None, nbytes, blocks, inflight, runs,
+                                  ctypes.c_void_p(sink) if sink else None, None)
+
+    assert call(buf=0) == NULL and call(sink=0) == NULL
+    assert call(nbytes=0) == SHAPE and call(nbytes=(1 << 20) + 8) == SHAPE and call(nbytes=(1 << 30) + 16) == SHAPE
+    assert call(blocks=0) == SHAPE and call(blocks=65537) == SHAPE
+    assert call(inflight=2) == RANGE and call(inflight=32) == RANGE and call(runs=2) == RANGE
+    assert call(buf=A + 8) == ALIGN and call(sink=A * 2 + 2) == ALIGN
