@@ -248,9 +248,10 @@ cats_status cats_mlp_forward_unfused(const cats_layer* layer, const float* x, in
  *   aux      per row, ascending: active_idx [B x d] kept channels,
  *            active_cnt [B], active_v = active_h [B x d] their values; or NULL
  * t >= 0; t = 0 keeps every channel (the dense product).  Workspace:
- * cats_sparse_input_workspace_bytes(d, n, B).  Enqueue only.  Not for graph
- * capture: the blocks' cross-block sum tags its counters with a value the
- * host draws per call, which a replayed graph would repeat. */
+ * cats_sparse_input_workspace_bytes(d, n, B).  Enqueue only; may be captured
+ * in a graph (the cross-block sum's counters carry a tag the host draws per
+ * call, and the last block of each column tile returns its counter to zero
+ * under that tag, so replays of one captured call and eager calls mix). */
 size_t cats_sparse_input_workspace_bytes(int32_t d, int32_t n, int32_t max_batch);
 cats_status cats_sparse_input_gemv(const void* w, int32_t d, int32_t n, int32_t wdtype,
                                    const float* x, int32_t B, float t, const float* residual,

@@ -20,7 +20,9 @@
 // y.  No block waits for another: the ticket is a compare-and-swap on a
 // word tagged with this call's epoch, so leftovers of earlier calls in the
 // workspace are simply restarted, and the loop only repeats when another
-// block's swap succeeded (at most NG times).
+// block's swap succeeded (at most NG times).  The last block puts the count
+// back to zero under the same tag, so a replayed graph, which repeats the
+// epoch it was captured with, finds its tickets fresh too.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -245,6 +247,10 @@ __global__ __launch_bounds__(kSThreads) void k_sparse_input(SparseInputArgs a) {
         break;
     }
     s_last = (int)(want & 0xffffffffull) == NG;
+    // The tile's count is complete: return it to zero under the same tag,
+    // so a call that repeats this epoch (a replayed graph) starts afresh.
+    if (s_last)
+      __hip_atomic_store(tk, (unsigned long long)a.epoch << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
   if (!s_last || !item) return;

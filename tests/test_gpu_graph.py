@@ -117,3 +117,23 @@ def test_unfused_graph(layers, mode):
                   lambda: P.mlp_forward_unfused(layer, x_static, 0.15, mode=mode, out=y_static, ws=ws),
                   x_static, y_static, lambda x: P.mlp_forward_unfused(layer, x, 0.15, mode=mode, ws=ws_e),
                   _inputs(B, 1024, REPLAYS, 70))
+
+
+@pytest.mark.parametrize("B,shared", [(1, False), (3, False), (3, True)])
+def test_sparse_input_graph(B, shared):
+    """The sparse-input product at n = 1024 (8 column tiles of 32 channel
+    groups: the cross-block sum with tickets).  With shared=True the eager
+    calls between replays use the captured call's own workspace, so replays
+    meet tickets left by calls with other tags."""
+    d, n = 2048, 1024
+    g = torch.Generator().manual_seed(80 + B)
+    w = (torch.randn((d, n), generator=g) * 0.02).to(torch.bfloat16).cuda()
+    x_static = torch.zeros((B, d), device="cuda")
+    y_static = torch.empty((B, n), device="cuda")
+    ws = P.sparse_input_workspace(d, n, B)
+    ws_e = ws if shared else P.sparse_input_workspace(d, n, B)
+    t = 0.6
+    _replay_check(f"sparse input B{B} shared={shared}",
+                  lambda: P.sparse_input_gemv(w, x_static, t, out=y_static, ws=ws),
+                  x_static, y_static, lambda x: P.sparse_input_gemv(w, x, t, ws=ws_e),
+                  _inputs(B, d, REPLAYS, 90 + B))
