@@ -672,9 +672,15 @@ def main() -> int:
             tsum += time.perf_counter() - t1
             bsum += req_bytes(int(r["cnt"][0]))
             n += 1
+        cpu = "unknown CPU"
+        try:
+            with open("/proc/cpuinfo") as f:
+                cpu = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), cpu)
+        except OSError:
+            pass
         out["cpu_baseline"] = {
             "value": round(bsum / tsum / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n} tokens of the {cfg.name} layer at k={k}, fp32 oracle, 1 thread "
+            "sample": f"{n} tokens of the {cfg.name} layer at k={k}, fp32 oracle, 1 thread of {cpu} "
                       f"({tsum * 1e3 / n:.1f} ms per token)",
         }
 
