@@ -1,0 +1,113 @@
+"""Run-to-run determinism at the full Llama2-7B-shaped size.
+
+Every cross-wave and cross-block sum in the library runs in a fixed order
+(no floating-point atomics), so repeated calls on the same inputs must give
+the same bits, whatever the workspace held before: each case calls three
+times, the last time with a workspace filled with garbage, and compares y
+(and the per-row active lists where the call returns them) bit for bit.
+A race in an LDS staging step or in a reduction shows up here as a
+difference between calls.
+"""
+import pytest
+import torch
+
+import paper_2404_08763_amd as P
+from paper_2404_08763_amd import workloads as W
+
+from gpu_util import device_layer, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def c2():
+    assert torch.cuda.is_available(), "GPU tests need a device"
+    c = W.CONFIGS["C2"]
+    wg, wu, wd = W.weights(c.d, c.m, c.wdtype)
+    return c, device_layer(wg, wu, wd)
+
+
+def _garbage_like(ws):
+    return torch.full_like(ws, 0xA5)
+
+
+def _same(a, b, label):
+    assert torch.equal(a.contiguous().view(torch.int32), b.contiguous().view(torch.int32)), label
+
+
+def _same_lists(a1, a2, B, label):
+    _same(a1["cnt"], a2["cnt"], label + " cnt")
+    for b in range(B):
+        n = int(a1["cnt"][b])
+        for k in ("idx", "v", "h"):
+            _same(a1[k][b, :n], a2[k][b, :n], f"{label} {k} row {b}")
+
+
+@pytest.mark.parametrize("B", [1, 4, 16])
+def test_forward_deterministic(c2, B):
+    """B = 1 and 4: the fused kernel; B = 16: the matrix-core path."""
+    c, layer = c2
+    x = W.decode_vectors(c, B).cuda()
+    t = 0.27
+    ws = P.workspace(c.d, c.m, B)
+    say("determinism forward B", B)
+    y1, a1 = P.mlp_forward(layer, x, t, ws=ws, aux=True)
+    y2, a2 = P.mlp_forward(layer, x, t, ws=ws, aux=True)
+    y3, a3 = P.mlp_forward(layer, x, t, ws=_garbage_like(ws), aux=True)
+    for y, a, lab in ((y2, a2, "repeat"), (y3, a3, "garbage workspace")):
+        _same(y1, y, f"B{B} {lab} y")
+        _same_lists(a1, a, B, f"B{B} {lab}")
+    _same(y1, P.mlp_forward(layer, x, t, ws=ws), f"B{B} without lists")
+
+
+def test_dense_deterministic(c2):
+    c, layer = c2
+    x = W.decode_vectors(c, 8).cuda()
+    ws = P.workspace(c.d, c.m, 8)
+    say("determinism dense B 8")
+    y1 = P.mlp_dense(layer, x, ws=ws)
+    _same(y1, P.mlp_dense(layer, x, ws=ws), "dense repeat")
+    _same(y1, P.mlp_dense(layer, x, ws=_garbage_like(ws)), "dense garbage workspace")
+
+
+@pytest.mark.parametrize("B", [1, 3])
+def test_topk_deterministic(c2, B):
+    c, layer = c2
+    x = W.decode_vectors(c, B).cuda()
+    nb = int(P.raw().cats_topk_workspace_bytes(c.d, c.m, B))
+    ws = torch.zeros(nb, dtype=torch.uint8, device="cuda")
+    say("determinism top-k B", B)
+    y1, t1 = P.mlp_forward_topk(layer, x, 0.7, ws=ws)
+    y2, t2 = P.mlp_forward_topk(layer, x, 0.7, ws=_garbage_like(ws))
+    _same(y1, y2, f"top-k B{B} y")
+    _same(t1, t2, f"top-k B{B} t")
+
+
+@pytest.mark.parametrize("mode", ["mask", "index"])
+@pytest.mark.parametrize("B", [1, 16])
+def test_unfused_deterministic(c2, mode, B):
+    c, layer = c2
+    x = W.decode_vectors(c, B).cuda()
+    nb = int(P.raw().cats_unfused_workspace_bytes(c.d, c.m, B))
+    ws = torch.zeros(nb, dtype=torch.uint8, device="cuda")
+    say("determinism unfused", mode, "B", B)
+    y1 = P.mlp_forward_unfused(layer, x, 0.27, mode=mode, ws=ws)
+    _same(y1, P.mlp_forward_unfused(layer, x, 0.27, mode=mode, ws=ws), f"unfused {mode} B{B} repeat")
+    _same(y1, P.mlp_forward_unfused(layer, x, 0.27, mode=mode, ws=_garbage_like(ws)),
+          f"unfused {mode} B{B} garbage workspace")
+
+
+@pytest.mark.parametrize("B", [1, 3])
+def test_sparse_input_deterministic(B):
+    """n = 1024: 8 column tiles of 32 channel groups, summed by the last
+    group of each tile (tickets)."""
+    d, n = 4096, 1024
+    g = torch.Generator().manual_seed(400 + B)
+    w = (torch.randn((d, n), generator=g) * 0.02).to(torch.bfloat16).cuda()
+    x = torch.randn((B, d), generator=g).cuda()
+    ws = P.sparse_input_workspace(d, n, B)
+    say("determinism sparse input B", B)
+    y1, a1 = P.sparse_input_gemv(w, x, 0.6, ws=ws, aux=True)
+    y2, a2 = P.sparse_input_gemv(w, x, 0.6, ws=_garbage_like(ws), aux=True)
+    _same(y1, y2, f"sparse input B{B} y")
+    _same_lists(a1, a2, B, f"sparse input B{B}")
