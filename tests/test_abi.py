@@ -328,3 +328,42 @@ def test_stream_read_validation():
     assert call(blocks=0) == SHAPE and call(blocks=65537) == SHAPE
     assert call(inflight=2) == RANGE and call(inflight=32) == RANGE and call(runs=2) == RANGE
     assert call(buf=A + 8) == ALIGN and call(sink=A * 2 + 2) == ALIGN
+
+
+def test_header_is_plain_c_and_links(tmp_path):
+    """include/cats.h compiles as strict C99 with every warning an error, and
+    a C program links against libcats.so and calls it (host-side paths only:
+    version, status strings, workspace sizing, validation before any HIP
+    call): the boundary needs neither C++ nor Python nor torch."""
+    import shutil
+    import subprocess
+
+    cc = shutil.which("gcc")
+    if cc is None:
+        pytest.skip("gcc not available")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    lib = P.lib_path()
+    src = tmp_path / "use_cats.c"
+    src.write_text(r'''
+#include "cats.h"
+#include <stdio.h>
+#include <string.h>
+int main(void) {
+  cats_layer layer;
+  memset(&layer, 0, sizeof layer);
+  layer.d = 4096;
+  layer.m = 11008;
+  layer.wdtype = CATS_BF16;
+  const size_t ws = cats_workspace_bytes(4096, 11008, 1, 0);
+  const cats_status st = cats_mlp_forward(&layer, NULL, 1, 0.5f, NULL, NULL, NULL, NULL, ws, NULL);
+  printf("%d %zu %d %s\n", (int)cats_version(), ws, (int)st, cats_status_string(st));
+  return (cats_version() == CATS_VERSION && ws > 0 && st == CATS_ERR_NULL) ? 0 : 1;
+}
+''')
+    exe = tmp_path / "use_cats"
+    libdir = os.path.dirname(lib)
+    subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", os.path.join(root, "include"),
+                    str(src), "-o", str(exe), "-L", libdir, "-l:" + os.path.basename(lib), "-Wl,-rpath," + libdir],
+                   check=True, capture_output=True, text=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True, timeout=60).stdout.split()
+    assert out[0] == str(P.raw().cats_version()) and int(out[1]) > 0 and int(out[2]) == NULL
