@@ -128,6 +128,16 @@ __device__ __forceinline__ uint32_t uniform_u32(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
 }
 
+// bf16 bit pattern nearest to f (ties to even); NaN stays a quiet NaN.
+// x = bf16(x) + bf16(x - bf16(x)) holds 16 of fp32's 24 significand bits,
+// and a bf16 weight times either part is exact in fp32: the split the
+// matrix-core paths use for fp32 inputs.
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t rne = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  return ((u & 0x7fffffffu) > 0x7f800000u) ? ((u >> 16) | 0x40u) : rne;
+}
+
 // SiLU(z) = z / (1 + e^{-z}).  For z below about -88 e^{-z} overflows to
 // +inf and the result is -0, whose magnitude 0 is masked by any t > 0.
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }

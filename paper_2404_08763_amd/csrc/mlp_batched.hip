@@ -41,13 +41,6 @@ constexpr int kGW = kGateUpWaves;
 constexpr int kGThreads = kGW * kWaveSize;
 constexpr int kBTileN = 16;  // neurons per MFMA tile (and batch columns)
 
-// bf16 bit pattern nearest to f (ties to even); NaN stays a quiet NaN.
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-  const uint32_t u = __float_as_uint(f);
-  const uint32_t rne = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-  return ((u & 0x7fffffffu) > 0x7f800000u) ? ((u >> 16) | 0x40u) : rne;
-}
-
 __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& v) { return __builtin_bit_cast(bf16x8, v); }
 
 // Split 8 fp32 values into bf16 hi and lo parts, packed two per word
