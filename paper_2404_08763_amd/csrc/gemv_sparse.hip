@@ -184,7 +184,12 @@ __global__ __launch_bounds__(kSThreads) void k_sparse_input(SparseInputArgs a) {
     seg_base += kept;
     __syncthreads();  // s_j / s_h are rewritten by the next round
   }
-  if (seg_writer && tid == 0) a.seg_cnt[q] = seg_base;
+  if (seg_writer) {
+    // the rest of the group's segment holds no channel: zero row masks, so
+    // a list entry is exactly an entry with its row's bit set
+    for (int e = c0 + seg_base + tid; e < c1; e += kSThreads) a.seg_mask[e] = 0u;
+    if (tid == 0) a.seg_cnt[q] = seg_base;
+  }
 
   // ---- the wave's RPL rows (lanes LPR r + chunk: rotations within each
   // row of 16 lanes for strides below 16, swaps across rows above), then

@@ -258,6 +258,9 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
     __syncthreads();
   }
   if (tid == 0) a.seg_cnt[blk] = base;
+  // the rest of the block's segment names no neuron: zero row masks, so a
+  // list entry is exactly an entry with its row's bit set
+  for (int i = base + tid; i < nb; i += kGThreads) a.seg_mask[n0 + i] = 0u;
 }
 
 // Down-projection on the matrix cores (5..16 rows). Block (ct, q) owns

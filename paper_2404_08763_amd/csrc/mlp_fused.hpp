@@ -301,6 +301,9 @@ __global__ __launch_bounds__(fused_waves(NCH, BT, VIN)* kWaveSize) void k_mlp_fu
   }
   if constexpr (AUX) {
     if (tid == 0) a.seg_cnt[blk] = nact;
+    // the rest of the block's segment names no neuron: zero row masks, so a
+    // list entry is exactly an entry with its row's bit set
+    for (int i = nact + tid; i < nb; i += NT) a.seg_mask[n0 + i] = 0u;
   }
 
   // ---- phase 3: down-projection, columns split over the waves

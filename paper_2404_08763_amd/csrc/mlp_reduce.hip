@@ -20,6 +20,13 @@ constexpr int kFinPer = 8;
 constexpr int kFinPass = kFinPer * kReduceThreads;
 constexpr int kFinCounts = kFinPer * kReduceWaves;
 static_assert(kFinCounts == kWaveSize, "one wave scans a pass's counts");
+// Blocks per row: ranges of about kFinRange entries (one compaction pass of
+// kFinPass covers a range); the count before a range reads kFinCountPer
+// masks per thread at a time.
+constexpr int kFinRange = 2048;
+constexpr int kFinCountPer = 32;
+constexpr int kFinCountPass = kFinCountPer * kReduceThreads;
+__host__ __device__ constexpr int fin_blocks(int m) { return m > kFinRange ? (m + kFinRange - 1) / kFinRange : 1; }
 
 __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
   const int tid = threadIdx.x;
@@ -70,20 +77,26 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
     return;
   }
 
-  // Finalize the active lists of row b.  Entry p of the segment arrays
-  // belongs to segment g(p), the last one whose start floor(g m / Gseg) is
-  // at most p, and names a union-active neuron when it is among the first
-  // seg_cnt[g] entries of its segment.  Segments are ascending and in neuron
-  // order, so row b's list is the named entries with bit b set, taken in
-  // order of p: an ordered stream compaction.  A pass covers kFinPass entries, kFinPer per thread at a
-  // stride of the block (coalesced); a ballot counts each wave's 64 entries
-  // of a pass and one wave scans the pass's 64 counts in entry order.
-  __shared__ int s_base[kFusedBlocks + 1];  // segment starts floor(g m / Gseg)
-  __shared__ int s_end[kFusedBlocks];       // ends of the segments' named entries
+  // Finalize the active lists.  Segment g (one per block of the producing
+  // kernel) covers entries [floor(g m / Gseg), floor((g + 1) m / Gseg)) of
+  // the segment arrays; its first seg_cnt[g] entries name the block's
+  // union-active neurons in ascending order with their row masks, and the
+  // producer zeroes the masks of the rest.  Segments are in neuron order, so
+  // row b's list is the entries with bit b set, taken in order: an ordered
+  // stream compaction.  A row's entries are split into fin_blocks(m) ranges,
+  // one block each.  A block first counts the row's list entries before its
+  // range (masks only, a pass's loads all in flight, one block sum), then
+  // compacts its own range from that offset: kFinPer entries per thread at
+  // a stride of the block (coalesced), a ballot counting each wave's 64
+  // entries of a pass and one wave scanning the pass's 64 counts in entry
+  // order.  No block waits for another.
   __shared__ int s_off[kFinCounts + 1];
-  const int b = blockIdx.x - nred;
+  const int m = a.m;
+  const int nfb = fin_blocks(m);
+  const int fi = blockIdx.x - nred;
+  const int b = fi / nfb, part = fi - b * nfb;
+  const int p_lo = (int)(((int64_t)part * m) / nfb), p_hi = (int)(((int64_t)(part + 1) * m) / nfb);
   const int w = tid / kWaveSize;
-  const int G = a.Gseg, m = a.m;
   const uint32_t mb = (uint32_t)m * 4u;
   const __amdgpu_buffer_rsrc_t rm = make_rsrc(a.seg_mask, mb);
   const __amdgpu_buffer_rsrc_t rj = make_rsrc(a.active_idx ? a.seg_j : nullptr, a.active_idx ? mb : 0u);
@@ -92,38 +105,53 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
   const __amdgpu_buffer_rsrc_t rh =
       make_rsrc(a.active_h ? a.seg_h + (size_t)b * m : nullptr, a.active_h ? mb : 0u);
   const uint64_t below = (1ull << lane) - 1ull;
-  const float gm = (float)G / (float)m;
+  auto listed = [&](uint32_t mk) -> bool { return (mk >> b) & 1u; };
+
+  int run = 0;  // list entries of row b before the current pass
+  {
+    int cnt = 0;
+    for (int p0 = 0; p0 < p_lo; p0 += kFinCountPass) {
+      uint32_t mk[kFinCountPer];
+#pragma unroll
+      for (int k = 0; k < kFinCountPer; ++k) {
+        const int p = p0 + k * kReduceThreads + tid;
+        mk[k] = __builtin_amdgcn_raw_buffer_load_b32(rm, p < p_lo ? (uint32_t)p * 4u : kOOB, 0, 0);
+      }
+#pragma unroll
+      for (int k = 0; k < kFinCountPer; ++k) {
+        const int p = p0 + k * kReduceThreads + tid;
+        cnt += (p < p_lo && listed(mk[k])) ? 1 : 0;
+      }
+    }
+#pragma unroll
+    for (int o = kWaveSize / 2; o >= 1; o >>= 1) cnt += __shfl_xor(cnt, o);
+    if (lane == 0) s_off[w] = cnt;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kReduceWaves; ++k) run += s_off[k];
+    __syncthreads();  // s_off is rewritten below
+  }
+
   struct Pass {
     uint32_t mk[kFinPer], jv[kFinPer], vv[kFinPer], hv[kFinPer];
   };
-  auto load = [&](Pass& f, int p0) {  // entries past m read as zero, no traffic
+  auto load = [&](Pass& f, int p0) {  // entries past the range read as zero, no traffic
 #pragma unroll
     for (int k = 0; k < kFinPer; ++k) {
       const int p = p0 + k * kReduceThreads + tid;
-      const uint32_t off = p < m ? (uint32_t)p * 4u : kOOB;
+      const uint32_t off = p < p_hi ? (uint32_t)p * 4u : kOOB;
       f.mk[k] = __builtin_amdgcn_raw_buffer_load_b32(rm, off, 0, 0);
       f.jv[k] = __builtin_amdgcn_raw_buffer_load_b32(rj, off, 0, 0);
       f.vv[k] = __builtin_amdgcn_raw_buffer_load_b32(rv, off, 0, 0);
       f.hv[k] = __builtin_amdgcn_raw_buffer_load_b32(rh, off, 0, 0);
     }
   };
-  int run = 0;  // list entries of row b before the current pass
   auto compact = [&](const Pass& f, int p0) {
     uint64_t bal[kFinPer];
 #pragma unroll
     for (int k = 0; k < kFinPer; ++k) {
       const int p = p0 + k * kReduceThreads + tid;
-      bool keep = false;
-      if (p < m) {
-        // g(p) from an fp32 estimate (off by at most one where segments are
-        // wider than one entry), moved to the last segment starting at or
-        // before p
-        int g = min((int)((float)p * gm), G - 1);
-        while (g + 1 < G && s_base[g + 1] <= p) ++g;
-        while (s_base[g] > p) --g;
-        keep = p < s_end[g] && ((f.mk[k] >> b) & 1u);
-      }
-      bal[k] = __ballot(keep);
+      bal[k] = __ballot(p < p_hi && listed(f.mk[k]));
       if (lane == 0) s_off[k * kReduceWaves + w] = __popcll(bal[k]);
     }
     __syncthreads();
@@ -153,28 +181,22 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
   };
   // The next pass's loads are in flight while a pass is compacted.
   Pass fa, fb;
-  load(fa, 0);
-  for (int g = tid; g <= G; g += kReduceThreads) {
-    const int base = (int)(((int64_t)g * m) / G);
-    s_base[g] = base;
-    if (g < G) s_end[g] = base + a.seg_cnt[g];
-  }
-  __syncthreads();
-  for (int p0 = 0; p0 < m; p0 += 2 * kFinPass) {
+  load(fa, p_lo);
+  for (int p0 = p_lo; p0 < p_hi; p0 += 2 * kFinPass) {
     load(fb, p0 + kFinPass);
     compact(fa, p0);
-    if (p0 + kFinPass < m) {
+    if (p0 + kFinPass < p_hi) {
       load(fa, p0 + 2 * kFinPass);
       compact(fb, p0 + kFinPass);
     }
   }
-  if (tid == 0 && a.active_cnt) a.active_cnt[b] = run;
+  if (tid == 0 && a.active_cnt && part == nfb - 1) a.active_cnt[b] = run;
 }
 
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s) {
   const int d4 = a.d >> 2;
   const int ncb = (d4 + kReduceWaves - 1) / kReduceWaves;
-  const int grid = (a.sum_y ? a.B * ncb : 0) + (a.aux ? a.B : 0);
+  const int grid = (a.sum_y ? a.B * ncb : 0) + (a.aux ? a.B * fin_blocks(a.m) : 0);
   if (grid == 0) return hipSuccess;
   KernelTimer timer("k_mlp_reduce", s);
   hipExtLaunchKernelGGL(k_mlp_reduce, dim3(grid), dim3(kReduceThreads), 0, s, timer.start(), timer.stop(), 0,
