@@ -56,7 +56,7 @@ __global__ __launch_bounds__(fused_waves(NCH, BT, VIN)* kWaveSize) void k_mlp_fu
 
   __shared__ __attribute__((aligned(16))) float xs[BT * DP];
   __shared__ float l_h[NBMAX][BT];   // h of each local neuron (0 where masked)
-  __shared__ float l_v[AUX ? NBMAX : 1][BT];
+  __shared__ float l_v[(AUX || VIN) ? NBMAX : 1][BT];  // v of each local neuron (VIN: as given)
   __shared__ uint32_t l_mask[NBMAX];  // row mask of each local neuron
   __shared__ int c_j[NBMAX];          // compacted: neuron index
   __shared__ float c_h[NBMAX][BT];    // compacted: h per batch row
@@ -157,6 +157,13 @@ __global__ __launch_bounds__(fused_waves(NCH, BT, VIN)* kWaveSize) void k_mlp_fu
       const int i4 = tid + k * NT;
       if (NV % NT == 0 || i4 < NV) *reinterpret_cast<u32x4*>(xs + i4 * 4) = xv[k];
     }
+    // VIN: the block's v values go to LDS with x, so a neuron's mask (and
+    // with it the decision to load its up row) does not wait for a load of
+    // its own v
+    if constexpr (VIN) {
+      for (int b = 0; b < B; ++b)
+        for (int loc = tid; loc < nb; loc += NT) l_v[loc][b] = a.vin[(size_t)b * m + n0 + loc];
+    }
   }
   __syncthreads();
 
@@ -199,10 +206,9 @@ __global__ __launch_bounds__(fused_waves(NCH, BT, VIN)* kWaveSize) void k_mlp_fu
     for (int b = 0; b < BT; ++b) v[b] = 0.f;
     if (i < ni) {
       if constexpr (VIN) {
-        const int j = n0 + w + i * W;
 #pragma unroll
         for (int b = 0; b < BT; ++b)
-          if (b < B) v[b] = a.vin[(size_t)b * m + j];
+          if (b < B) v[b] = l_v[w + i * W][b];
       } else {
         float g[BT];
         row_dot(gcur, g);
