@@ -388,6 +388,56 @@ def bench_ablation(P, W, torch, timed, cfg_name, steps, warm, rotate, layers=Non
     return out
 
 
+def bench_shards(P, torch, timed, layers, xs, thr, ks, steps, warm):
+    """One GPU's share of the benchmark layer when the neurons are split over
+    N GPUs (the first m / N neurons of each rotated copy: a neuron shard is
+    its rows of all three neuron-major matrices), at the layer's cutoffs;
+    the cross-GPU sum of the partial outputs is not part of this."""
+    import numpy as np
+
+    d, m = layers[0].d, layers[0].m
+    R, ntok = len(layers), xs.shape[0]
+    sw = layers[0].w_gate_t.element_size()
+    L = P.raw()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    xptr = [ctypes.c_void_p(xs[i : i + 1].data_ptr()) for i in range(ntok)]
+    y = torch.empty((1, d), dtype=torch.float32, device=xs.device)
+    yptr = ctypes.c_void_p(y.data_ptr())
+    out = {"workload": "one neuron shard of the benchmark layer, batch 1 (its rows of all three matrices)"}
+    for n in (2, 4, 8):
+        ms = m // n
+        shard = [P.Layer(l.w_gate_t[:ms].contiguous(), l.w_up_t[:ms].contiguous(), l.w_down[:ms].contiguous())
+                 for l in layers]
+        ws = P.workspace(d, ms, 1)
+        wsp, wsn = ctypes.c_void_p(ws.data_ptr()), ws.numel()
+
+        def call(s, t, shard=shard, wsp=wsp, wsn=wsn):
+            st = L.cats_mlp_forward(shard[s % R].c, xptr[s % ntok], 1, ctypes.c_float(t), None, yptr, None, wsp,
+                                    wsn, stream)
+            if st != 0:
+                raise P.CatsError(st, L.cats_last_error().decode())
+
+        def dense(s, shard=shard, wsp=wsp, wsn=wsn):
+            st = L.cats_mlp_dense(shard[s % R].c, xptr[s % ntok], 1, None, yptr, wsp, wsn, stream)
+            if st != 0:
+                raise P.CatsError(st, L.cats_last_error().decode())
+
+        row = {"m": ms}
+        for k in ks:
+            nact = np.zeros(ntok, np.int64)
+            for i in range(ntok):
+                _, aux = P.mlp_forward(shard[0], xs[i : i + 1], thr[k], ws=ws, aux=True)
+                nact[i] = int(aux["cnt"][0])
+            ms_k = timed(lambda s, k=k: call(s, thr[k]), warm, steps)
+            nb = sum(sw * d * (ms + 2 * int(nact[(warm + s) % ntok])) + 8 * d for s in range(steps))
+            row[str(k)] = {"us": round(ms_k * 1e3 / steps, 3), "gbps": round(nb / (ms_k * 1e-3) / 1e9, 1)}
+        ms_d = timed(dense, warm, steps)
+        row["dense_us"] = round(ms_d * 1e3 / steps, 3)
+        out[f"n{n}"] = row
+        del shard, ws
+    return out
+
+
 def bench_topk(P, W, torch, timed, layers, xs, ks, dense_us, steps, warm):
     """Per-token top-k variant on the benchmark layer: row b keeps the
     neurons at or above the r-th smallest of its own |v| (r = ceil(k m)),
@@ -636,6 +686,8 @@ def main() -> int:
         log(f"[bench] attainable read {att}")
         out["kernel_avg_us"] = {n: round(v[1] * 1e3 / v[0], 3) for n, v in kt.items() if v[0]}
         out["timed_region_with_kernel_events_ms_per_step"] = round(ms_timer / K, 5)
+        out["shards"] = bench_shards(P, torch, timed, layers, xs, thr, ks, K, Wm)
+        log(f"[bench] neuron shards: {out['shards']}")
         out["topk"] = bench_topk(P, W, torch, timed, layers, xs, ks, dense_us, K, Wm)
         log(f"[bench] top-k: {out['topk']}")
         out["ablation_" + cfg.name] = bench_ablation(P, W, torch, timed, cfg.name, K, Wm, R, layers,
