@@ -129,7 +129,10 @@ cats_status cats_pack_weights(const void* w, void* w_t, int32_t rows, int32_t co
 
 /* Calibration activations (Section 4.1): for N vectors x_n (dev [N x d],
  * fp32) writes acts[n*m + j] = |SiLU(x_n . W_gate[:, j])| (dev [N x m]).
- * Enqueue only. */
+ * fp32 accumulation; with bf16 weights the products run on the matrix
+ * cores with x split into two bf16 parts (16 of its 24 significand bits,
+ * each product exact), so a dot product differs from an fp32 one by about
+ * 2^-16 of its absolute terms.  Enqueue only. */
 cats_status cats_calib_activations(const cats_layer* layer, const float* x, int32_t N,
                                    float* acts, void* stream);
 
