@@ -96,19 +96,22 @@ __global__ __launch_bounds__(256) void k_calib_acts(const float* __restrict__ X,
 }
 
 // bf16 weights: the same contraction on the matrix cores.  A block owns
-// 128 neurons x 128 calibration vectors; its four waves own 64 x 64 each,
+// 256 neurons x 128 calibration vectors; its eight waves own 64 x 64 each,
 // 4 x 4 MFMA tiles of 16 x 16 (A: 16 neurons x 32 k of W_gate^T, bf16 as
 // stored; B: 32 k x 16 vectors of x as bf16 hi + lo, two products per tile
 // and step into one fp32 accumulator).  The reduction runs through LDS 64 k
 // at a time; the next stage's global loads are in flight while a stage is
 // multiplied.  |SiLU| is applied to each accumulator in the epilogue.
-constexpr int kCmM = 128;            // neurons per block
+constexpr int kCmM = 256;            // neurons per block (128 x 128 took 0.81 ms at C2, 256 x 128 0.68)
 constexpr int kCmN = 128;            // calibration vectors per block
 constexpr int kCmK = 64;             // reduction depth per LDS stage
 constexpr int kCmPitch = kCmK + 8;   // bf16 per LDS row (16 B pad: rows 4 banks apart)
-constexpr int kCmThreads = 256;
+constexpr int kCmThreads = 512;
 constexpr int kCmWLoads = kCmM * kCmK * 2 / (16 * kCmThreads);  // 16-byte W loads per thread and stage
 constexpr int kCmXLoads = kCmN * kCmK * 4 / (16 * kCmThreads);  // 16-byte x loads per thread and stage
+
+static_assert(kCmN == 128 && (kCmM / 64) * (kCmN / 64) * kWaveSize == kCmThreads,
+              "waves form a (kCmM / 64) x 2 grid of 64 x 64 tiles");
 
 typedef __bf16 cm_bf16x8 __attribute__((ext_vector_type(8)));
 
@@ -119,11 +122,11 @@ __global__ __launch_bounds__(kCmThreads) void k_calib_acts_mfma(const float* __r
   __shared__ __attribute__((aligned(16))) uint16_t s_xh[kCmN][kCmPitch];
   __shared__ __attribute__((aligned(16))) uint16_t s_xl[kCmN][kCmPitch];
   const int tid = threadIdx.x, lane = tid & (kWaveSize - 1);
-  const int w = tid / kWaveSize, wm = w >> 1, wn = w & 1;
+  const int w = tid / kWaveSize, wm = w >> 1, wn = w & 1;  // 4 x 2 waves of 64 x 64
   const int r16 = lane & 15, kb = lane >> 4;
   const int j0 = blockIdx.x * kCmM, v0 = blockIdx.y * kCmN;
   const int rows_w = min(kCmM, m - j0), rows_x = min(kCmN, N - v0);
-  // per-block resources: at most 128 rows of either matrix (<= 4 MB)
+  // per-block resources: at most 256 rows of W (<= 4 MB) and 128 of x (<= 4 MB)
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wt + (size_t)j0 * d, (uint32_t)(rows_w * d * 2));
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + (size_t)v0 * d, (uint32_t)(rows_x * d * 4));
 
