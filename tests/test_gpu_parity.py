@@ -361,6 +361,27 @@ def test_full_size_forward(big, oracle32, name, ks):
             assert torch.equal(y.view(torch.int32), y_noaux.view(torch.int32))
 
 
+@pytest.mark.parametrize("n", [4, 8])
+def test_neuron_shard(big, oracle32, n):
+    """One GPU's share of the C2 block split by neuron over n GPUs (its first
+    m / n rows of all three neuron-major matrices), the shape the benchmark's
+    shard figures run: at one row each wave owns two or three neurons."""
+    c, layer, hw = big("C2")
+    ms = c.m // n
+    shard = P.Layer(layer.w_gate_t[:ms].contiguous(), layer.w_up_t[:ms].contiguous(),
+                    layer.w_down[:ms].contiguous())
+    hws = [np.ascontiguousarray(hw[0][:, :ms]), np.ascontiguousarray(hw[1][:, :ms]),
+           np.ascontiguousarray(hw[2][:ms])]
+    for B in (1, 3):
+        x = W.decode_vectors(c, B).numpy()
+        ref_all = oracle32.cats_mlp(x, *hws, t=0.0)
+        t = quantile_t(np.abs(ref_all["v"]), 0.5)
+        say("C2 shard 1 /", n, "B", B, "t", t)
+        y, aux = P.mlp_forward(shard, torch.from_numpy(x).cuda(), t, aux=True)
+        ref = oracle32.cats_mlp(x, *hws, t=t)
+        check_forward(y, aux, ref, t, B, f"C2 shard 1/{n} B{B}", ref_all=ref_all, w_down=hws[2])
+
+
 def test_full_size_dense(big, oracle32):
     c, layer, hw = big("C2")
     x = W.decode_vectors(c, 1)
