@@ -21,6 +21,8 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcats.so
 
 CATS_F32 = 0
 CATS_BF16 = 1
+# size of the fixed scratch array behind cats_mlp_forward_noalloc
+NOALLOC_SCRATCH_BYTES = 32 << 20
 STATUS_NAMES = {
     0: "CATS_OK", 1: "CATS_ERR_NULL", 2: "CATS_ERR_SHAPE", 3: "CATS_ERR_RANGE",
     4: "CATS_ERR_DTYPE", 5: "CATS_ERR_ALIGN", 6: "CATS_ERR_WORKSPACE", 7: "CATS_ERR_HIP",
@@ -64,6 +66,8 @@ _SIGNATURES = {
                                   ctypes.POINTER(_f32)], _i32),
     "cats_mlp_forward": ([ctypes.POINTER(_Layer), _vp, _i32, _f32, _vp, _vp, ctypes.POINTER(_Aux),
                           _vp, _sz, _vp], _i32),
+    "cats_mlp_forward_noalloc": ([ctypes.POINTER(_Layer), _vp, _i32, _f32, _vp, _vp, ctypes.POINTER(_Aux), _vp],
+                                 _i32),
     "cats_mlp_dense": ([ctypes.POINTER(_Layer), _vp, _i32, _vp, _vp, _vp, _sz, _vp], _i32),
     "cats_stack_forward": ([ctypes.POINTER(_Layer), _i32, ctypes.POINTER(_f32), _vp, _i32, _f32, _vp,
                             _vp, ctypes.POINTER(_Aux), _vp, _sz, _vp], _i32),
@@ -205,11 +209,13 @@ def layer_from_math(w_gate: torch.Tensor, w_up: torch.Tensor, w_down: torch.Tens
 
 
 def calib_activations(layer: Layer, x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    N = _rows_of(x, layer.d)
+    _numel_is(out, N * layer.m, "out")
     _dev(x, "x", torch.float32)
-    N = x.shape[0]
     if out is None:
         out = torch.empty((N, layer.m), dtype=torch.float32, device=x.device)
     _dev(out, "out", torch.float32)
+    _numel_is(out, N * layer.m, "out")
     _check(raw().cats_calib_activations(layer.c, _ptr(x), N, _ptr(out), _stream()))
     return out
 
@@ -226,8 +232,8 @@ def threshold_from_acts(acts: torch.Tensor, sparsity: float, ws: Optional[torch.
 
 def calibrate_threshold(layer: Layer, calib_x: torch.Tensor, sparsity: float,
                         ws: Optional[torch.Tensor] = None) -> float:
+    N = _rows_of(calib_x, layer.d, "calib_x")
     _dev(calib_x, "calib_x", torch.float32)
-    N = calib_x.shape[0]
     if ws is None:
         ws = workspace(layer.d, layer.m, 1, N * layer.m, device=calib_x.device)
     t = _f32()
@@ -240,6 +246,38 @@ def _rows(x: torch.Tensor) -> int:
     return 1 if x.dim() == 1 else int(x.shape[0])
 
 
+def _rows_of(x: torch.Tensor, d: int, name: str = "x") -> int:
+    """Rows of a [B, d] (or [d]) activation tensor; raises before any call
+    into the library when its width is not the layer's d, since the kernels
+    read and write B * d floats through raw pointers."""
+    if x.dim() not in (1, 2):
+        raise ValueError(f"{name} must be [d] or [B, d], got shape {tuple(x.shape)}")
+    if int(x.shape[-1]) != d:
+        raise ValueError(f"{name} has width {int(x.shape[-1])}, the layer has d={d}")
+    return _rows(x)
+
+
+def _numel_is(t: Optional[torch.Tensor], n: int, name: str) -> None:
+    if t is not None and t.numel() != n:
+        raise ValueError(f"{name} must hold {n} elements, has {t.numel()}")
+
+
+def _io_checks(x: torch.Tensor, d: int, out: Optional[torch.Tensor], residual: Optional[torch.Tensor],
+               n_out: Optional[int] = None) -> int:
+    """Validate x, out and residual of a [B, d] -> [B, n_out] call; returns B.
+    Shapes are checked first, so a mismatch raises whatever the device."""
+    B = _rows_of(x, d)
+    n_out = d if n_out is None else n_out
+    _numel_is(out, B * n_out, "out")
+    _numel_is(residual, B * n_out, "residual")
+    _dev(x, "x", torch.float32)
+    if out is not None:
+        _dev(out, "out", torch.float32)
+    if residual is not None:
+        _dev(residual, "residual", torch.float32)
+    return B
+
+
 def mlp_forward(layer: Layer, x: torch.Tensor, t: float, residual: Optional[torch.Tensor] = None,
                 out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
                 aux: bool = False):
@@ -248,13 +286,9 @@ def mlp_forward(layer: Layer, x: torch.Tensor, t: float, residual: Optional[torc
     The aux dict holds per row b: idx[b, :cnt[b]] (ascending active neurons),
     v and h (= v * x.W_up[:, j]) aligned with idx, and cnt.
     """
-    _dev(x, "x", torch.float32)
-    B = _rows(x)
+    B = _io_checks(x, layer.d, out, residual)
     if out is None:
         out = torch.empty_like(x)
-    _dev(out, "out", torch.float32)
-    if residual is not None:
-        _dev(residual, "residual", torch.float32)
     if ws is None:
         ws = workspace(layer.d, layer.m, B, device=x.device)
     aux_c = None
@@ -286,15 +320,11 @@ def mlp_forward_unfused(layer: Layer, x: torch.Tensor, t: float, mode: str = "ma
                         residual: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
                         ws: Optional[torch.Tensor] = None) -> torch.Tensor:
     """The forward in separate gate / up / down kernels; mode "mask" or "index"."""
-    _dev(x, "x", torch.float32)
-    B = _rows(x)
+    B = _io_checks(x, layer.d, out, residual)
     if mode not in _UNFUSED_MODES:
         raise ValueError(f"mode must be one of {sorted(_UNFUSED_MODES)}")
     if out is None:
         out = torch.empty_like(x)
-    _dev(out, "out", torch.float32)
-    if residual is not None:
-        _dev(residual, "residual", torch.float32)
     if ws is None:
         nbytes = int(raw().cats_unfused_workspace_bytes(layer.d, layer.m, B))
         if nbytes == 0:
@@ -308,13 +338,9 @@ def mlp_forward_unfused(layer: Layer, x: torch.Tensor, t: float, mode: str = "ma
 def mlp_forward_topk(layer: Layer, x: torch.Tensor, sparsity: float, residual: Optional[torch.Tensor] = None,
                      out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, aux: bool = False):
     """Per-token top-k variant.  Returns (y, t [B]) or (y, t, aux dict)."""
-    _dev(x, "x", torch.float32)
-    B = _rows(x)
+    B = _io_checks(x, layer.d, out, residual)
     if out is None:
         out = torch.empty_like(x)
-    _dev(out, "out", torch.float32)
-    if residual is not None:
-        _dev(residual, "residual", torch.float32)
     if ws is None:
         nbytes = int(raw().cats_topk_workspace_bytes(layer.d, layer.m, B))
         if nbytes == 0:
@@ -342,13 +368,9 @@ def mlp_forward_topk(layer: Layer, x: torch.Tensor, sparsity: float, residual: O
 
 def mlp_dense(layer: Layer, x: torch.Tensor, residual: Optional[torch.Tensor] = None,
               out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
-    _dev(x, "x", torch.float32)
-    B = _rows(x)
+    B = _io_checks(x, layer.d, out, residual)
     if out is None:
         out = torch.empty_like(x)
-    _dev(out, "out", torch.float32)
-    if residual is not None:
-        _dev(residual, "residual", torch.float32)
     if ws is None:
         ws = workspace(layer.d, layer.m, B, device=x.device)
     _check(raw().cats_mlp_dense(layer.c, _ptr(x), B, _ptr(residual), _ptr(out), _ptr(ws), ws.numel(),
@@ -385,8 +407,9 @@ def stack_forward(stack: Stack, x0: torch.Tensor, eps: float = 1e-5, out: Option
 
     Returns x_L, or a dict with "out", "x_all" [(L+1), B, d] (keep_all) and
     "aux" (a list of per-layer dicts as from mlp_forward, when aux=True)."""
+    B = _rows_of(x0, stack.d, "x0")
+    _numel_is(out, B * stack.d, "out")
     _dev(x0, "x0", torch.float32)
-    B = _rows(x0)
     L = len(stack)
     if out is None:
         out = torch.empty_like(x0)
@@ -420,8 +443,8 @@ def calibrate_stack(stack: Stack, calib_x: torch.Tensor, sparsity: float, eps: f
                     ws: Optional[torch.Tensor] = None) -> list:
     """Per-layer thresholds of a stack, the calibration vectors propagated
     densely through the earlier layers (cats_calibrate_stack)."""
+    N = _rows_of(calib_x, stack.d, "calib_x")
     _dev(calib_x, "calib_x", torch.float32)
-    N = _rows(calib_x)
     L = len(stack)
     if ws is None:
         n = int(raw().cats_calibrate_stack_workspace_bytes(stack.d, stack.max_m, N))
@@ -447,15 +470,13 @@ def sparse_input_gemv(w: torch.Tensor, x: torch.Tensor, t: float, residual: Opti
 
     Returns y, or (y, aux dict) with per row the ascending kept channels
     idx[b, :cnt[b]] and their values v (= h)."""
-    _dev(w, "w", torch.bfloat16)
-    _dev(x, "x", torch.float32)
+    if w.dim() != 2:
+        raise ValueError(f"w must be [d, n], got shape {tuple(w.shape)}")
     d, n = int(w.shape[0]), int(w.shape[1])
-    B = _rows(x)
+    B = _io_checks(x, d, out, residual, n_out=n)
+    _dev(w, "w", torch.bfloat16)
     if out is None:
         out = torch.empty((B, n), dtype=torch.float32, device=x.device)
-    _dev(out, "out", torch.float32)
-    if residual is not None:
-        _dev(residual, "residual", torch.float32)
     if ws is None:
         ws = sparse_input_workspace(d, n, B, device=x.device)
     aux_c = None
@@ -478,9 +499,12 @@ def sparse_input_gemv(w: torch.Tensor, x: torch.Tensor, t: float, residual: Opti
 
 def rmsnorm(x: torch.Tensor, eps: float = 1e-5, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     _dev(x, "x", torch.float32)
+    if x.dim() not in (1, 2):
+        raise ValueError(f"x must be [d] or [B, d], got shape {tuple(x.shape)}")
     if out is None:
         out = torch.empty_like(x)
     _dev(out, "out", torch.float32)
+    _numel_is(out, x.numel(), "out")
     B = _rows(x)
     d = int(x.shape[-1])
     _check(raw().cats_rmsnorm(_ptr(x), _ptr(out), B, d, float(eps), _stream()))
