@@ -166,6 +166,23 @@ cats_status cats_mlp_forward(const cats_layer* layer, const float* x, int32_t B,
                              const float* residual, float* y, const cats_forward_aux* aux,
                              void* ws, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the CATS
+ * forward above with the same arguments, semantics and kernels, minus the
+ * workspace.  Its scratch memory is a fixed array of
+ * CATS_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends; the call itself allocates nothing.  Blocks and
+ * batches whose cats_workspace_bytes(d, m, B, 0) exceeds that size are
+ * rejected with CATS_ERR_WORKSPACE before any device work (the batch-1
+ * forward fits up to d = 8192 with m = 28672; 4 rows at d = 4096,
+ * m = 11008).  Every call on one GPU shares that GPU's array: calls that
+ * overlap on one GPU (other streams, other threads) race and must be
+ * serialised by the caller.  Enqueue only. */
+#define CATS_NOALLOC_SCRATCH_BYTES (32u << 20)
+cats_status cats_mlp_forward_noalloc(const cats_layer* layer, const float* x, int32_t B, float t,
+                                     const float* residual, float* y, const cats_forward_aux* aux,
+                                     void* stream);
+
 /* Dense gated MLP (Eq. 1, every neuron kept): the comparison baseline
  * ("Dense" of Section 5.3).  Same arguments and layouts as the forward. */
 cats_status cats_mlp_dense(const cats_layer* layer, const float* x, int32_t B,

@@ -375,6 +375,10 @@ hipEvent_t timer_event_locked(TimerState& T) {
 
 }  // namespace
 
+namespace cats {
+cats_status report_error(cats_status st, const char* msg) { return fail(st, "%s", msg); }
+}  // namespace cats
+
 static_assert(CATS_MAX_M == cats::kMaxNeurons, "CATS_MAX_M must match the kernel's neuron capacity");
 
 namespace cats {
