@@ -8,7 +8,11 @@ it; the product library never does, and it shares no code with it.
 
 Two builds of the same source exist: ``f32`` (the paper runs everything in
 FP32) accumulates in float, ``f64`` in double.  Both sum every dot product
-in ascending index order from +0, without fused multiply-add.
+in ascending index order from +0, without fused multiply-add.  ``f32_omp``
+is the f32 build compiled with OpenMP: threads split independent outputs
+(neurons, output columns, calibration vectors), never a sum, so it returns
+the f32 build's bits on all the host's cores (a CPU baseline, not a
+reference).
 """
 from __future__ import annotations
 
@@ -32,6 +36,8 @@ def compile_oracle(out_path: str, source: str = SOURCE, precision: str = "f32") 
     flags = list(CFLAGS)
     if precision == "f64":
         flags.append("-DORACLE_F64")
+    elif precision == "f32_omp":
+        flags.append("-fopenmp")
     elif precision != "f32":
         raise ValueError(f"unknown oracle precision {precision!r}")
     cmd = ["gcc", *flags, "-I", _HERE, "-o", out_path, source, "-lm"]
@@ -40,8 +46,8 @@ def compile_oracle(out_path: str, source: str = SOURCE, precision: str = "f32") 
 
 
 def build() -> None:
-    """Build both oracle precisions in place."""
-    for p in ("f32", "f64"):
+    """Build both oracle precisions and the OpenMP f32 build in place."""
+    for p in ("f32", "f64", "f32_omp"):
         compile_oracle(lib_path(p), precision=p)
 
 
@@ -66,6 +72,8 @@ class Oracle:
         self.path = path
         L = ctypes.CDLL(path)
         L.oracle_precision.restype = ctypes.c_char_p
+        L.oracle_threads.argtypes = [ctypes.c_int]
+        L.oracle_threads.restype = ctypes.c_int
         L.oracle_silu.argtypes = [ctypes.c_double]
         L.oracle_silu.restype = ctypes.c_double
         L.oracle_cats_mlp.argtypes = [_PF, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -95,6 +103,11 @@ class Oracle:
         L.oracle_threshold.restype = ctypes.c_int
         self._L = L
         self.precision = L.oracle_precision().decode()
+
+    def threads(self, n: int = 0) -> int:
+        """Set the thread count of an OpenMP build (n > 0); returns the count
+        in use (1 for a sequential build)."""
+        return int(self._L.oracle_threads(int(n)))
 
     def silu(self, z: float) -> float:
         return float(self._L.oracle_silu(float(z)))

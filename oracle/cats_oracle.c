@@ -25,6 +25,9 @@
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #ifdef ORACLE_F64
 typedef double real;
@@ -41,6 +44,34 @@ static const char* k_precision = "f32";
 #endif
 
 const char* oracle_precision(void) { return k_precision; }
+
+/* Threads: an OpenMP build (-fopenmp) splits independent outputs over
+ * threads -- the neurons of x W_gate and x W_up, the columns of the
+ * down-projection, the calibration vectors -- and never a sum, so every
+ * value is computed by the same operations in the same order as in the
+ * sequential build, bit for bit. */
+int oracle_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+  return omp_get_max_threads();
+#else
+  (void)n;
+  return 1;
+#endif
+}
+
+/* This thread's share [*lo, *hi) of n independent outputs (all of them in
+ * a sequential build or outside a parallel region). */
+static void thread_share(int32_t n, int32_t* lo, int32_t* hi) {
+#ifdef _OPENMP
+  const int64_t nt = omp_get_num_threads(), t = omp_get_thread_num();
+  *lo = (int32_t)(n * t / nt);
+  *hi = (int32_t)(n * (t + 1) / nt);
+#else
+  *lo = 0;
+  *hi = n;
+#endif
+}
 
 /* Eq. 2. */
 static real silu(real z) { return z / ((real)1 + R_EXP(-z)); }
@@ -61,26 +92,33 @@ int oracle_cats_mlp(const float* x, int32_t B, int32_t d, int32_t m,
   real* g = (real*)malloc(sizeof(real) * (size_t)m);
   real* u = (real*)malloc(sizeof(real) * (size_t)m);
   real* s = (real*)malloc(sizeof(real) * (size_t)d);
-  if (!g || !u || !s) { free(g); free(u); free(s); return -1; }
+  int32_t* act = (int32_t*)malloc(sizeof(int32_t) * (size_t)m);
+  real* hv = (real*)malloc(sizeof(real) * (size_t)m);
+  if (!g || !u || !s || !act || !hv) { free(g); free(u); free(s); free(act); free(hv); return -1; }
 
   for (int32_t b = 0; b < B; ++b) {
     const float* xb = x + (size_t)b * d;
     /* g = x W_gate and u = x W_up.  The loops run i outermost so that the
      * weights are read row by row; each g_j and u_j still accumulates its
      * d terms in ascending i, starting from +0. */
-    for (int32_t j = 0; j < m; ++j) { g[j] = 0; u[j] = 0; }
-    for (int32_t i = 0; i < d; ++i) {
-      const real xi = (real)xb[i];
-      const float* wg_row = w_gate + (size_t)i * m;
-      const float* wu_row = w_up + (size_t)i * m;
-      for (int32_t j = 0; j < m; ++j) {
-        g[j] += xi * (real)wg_row[j];
-        u[j] += xi * (real)wu_row[j];
+#ifdef _OPENMP
+#pragma omp parallel
+#endif
+    {
+      int32_t j0, j1;
+      thread_share(m, &j0, &j1);
+      for (int32_t j = j0; j < j1; ++j) { g[j] = 0; u[j] = 0; }
+      for (int32_t i = 0; i < d; ++i) {
+        const real xi = (real)xb[i];
+        const float* wg_row = w_gate + (size_t)i * m;
+        const float* wu_row = w_up + (size_t)i * m;
+        for (int32_t j = j0; j < j1; ++j) {
+          g[j] += xi * (real)wg_row[j];
+          u[j] += xi * (real)wu_row[j];
+        }
       }
     }
-    /* v = SiLU(g); Mask; x1 = u[Mask] * v[Mask]; s = x1 W_down[Mask].
-     * s_k accumulates the active j in ascending order, from +0. */
-    for (int32_t k = 0; k < d; ++k) s[k] = 0;
+    /* v = SiLU(g); Mask; x1 = u[Mask] * v[Mask], listed in ascending j. */
     int32_t cnt = 0;
     for (int32_t j = 0; j < m; ++j) {
       const real v = silu(g[j]);
@@ -89,18 +127,34 @@ int oracle_cats_mlp(const float* x, int32_t B, int32_t d, int32_t m,
       const real h = v * u[j];
       if (active_idx) active_idx[(size_t)b * m + cnt] = j;
       if (h_act) h_act[(size_t)b * m + cnt] = (double)h;
+      act[cnt] = j;
+      hv[cnt] = h;
       ++cnt;
-      const float* wd_row = w_down + (size_t)j * d;
-      for (int32_t k = 0; k < d; ++k) s[k] += h * (real)wd_row[k];
     }
     if (active_cnt) active_cnt[b] = cnt;
+    /* s = x1 W_down[Mask]: s_k accumulates the active j in ascending
+     * order, from +0. */
+#ifdef _OPENMP
+#pragma omp parallel
+#endif
+    {
+      int32_t k0, k1;
+      thread_share(d, &k0, &k1);
+      for (int32_t k = k0; k < k1; ++k) s[k] = 0;
+      for (int32_t q = 0; q < cnt; ++q) {
+        const int32_t j = act[q];
+        const real h = hv[q];
+        const float* wd_row = w_down + (size_t)j * d;
+        for (int32_t k = k0; k < k1; ++k) s[k] += h * (real)wd_row[k];
+      }
+    }
     for (int32_t k = 0; k < d; ++k) {
       real out = s[k];
       if (residual) out = (real)residual[(size_t)b * d + k] + out;
       y[(size_t)b * d + k] = (double)out;
     }
   }
-  free(g); free(u); free(s);
+  free(g); free(u); free(s); free(act); free(hv);
   return 0;
 }
 
@@ -214,21 +268,35 @@ static real calib_act(const float* xn, int32_t d, int32_t m, const float* w_gate
 int oracle_calib_acts(const float* X, int32_t N, int32_t d, int32_t m,
                       const float* w_gate, double* acts) {
   if (!X || !w_gate || !acts || N <= 0 || d <= 0 || m <= 0) return -1;
-  real* g = (real*)malloc(sizeof(real) * (size_t)m);
-  if (!g) return -1;
-  for (int32_t n = 0; n < N; ++n) {
-    const float* xn = X + (size_t)n * d;
-    /* Same ascending-i accumulation as calib_act, with i outermost. */
-    for (int32_t j = 0; j < m; ++j) g[j] = 0;
-    for (int32_t i = 0; i < d; ++i) {
-      const real xi = (real)xn[i];
-      const float* row = w_gate + (size_t)i * m;
-      for (int32_t j = 0; j < m; ++j) g[j] += xi * (real)row[j];
+  int failed = 0;
+#ifdef _OPENMP
+#pragma omp parallel
+#endif
+  {
+    real* g = (real*)malloc(sizeof(real) * (size_t)m);
+    int32_t n0, n1;
+    thread_share(N, &n0, &n1);
+    if (!g) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+      failed = 1;
+      n1 = n0;
     }
-    for (int32_t j = 0; j < m; ++j) acts[(size_t)n * m + j] = (double)R_FABS(silu(g[j]));
+    for (int32_t n = n0; n < n1; ++n) {
+      const float* xn = X + (size_t)n * d;
+      /* Same ascending-i accumulation as calib_act, with i outermost. */
+      for (int32_t j = 0; j < m; ++j) g[j] = 0;
+      for (int32_t i = 0; i < d; ++i) {
+        const real xi = (real)xn[i];
+        const float* row = w_gate + (size_t)i * m;
+        for (int32_t j = 0; j < m; ++j) g[j] += xi * (real)row[j];
+      }
+      for (int32_t j = 0; j < m; ++j) acts[(size_t)n * m + j] = (double)R_FABS(silu(g[j]));
+    }
+    free(g);
   }
-  free(g);
-  return 0;
+  return failed ? -1 : 0;
 }
 
 int oracle_calib_acts_at(const float* X, int32_t N, int32_t d, int32_t m,

@@ -33,6 +33,12 @@ extern "C" {
 /* Name of the accumulation type this copy was compiled with: "f32" or "f64". */
 const char* oracle_precision(void);
 
+/* Threads of an OpenMP build (-fopenmp): sets the count when n > 0 and
+ * returns the count in use (1 in a sequential build).  Threads split
+ * independent outputs only, so results are bit-identical to the
+ * sequential build. */
+int oracle_threads(int n);
+
 /* SiLU(z) = z / (1 + exp(-z)) (Eq. 2), evaluated in the build's precision. */
 double oracle_silu(double z);
 

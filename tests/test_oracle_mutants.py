@@ -22,13 +22,13 @@ MUTANTS = {
     # x1 = v instead of v * (x W_up)
     "drop_up": ("const real h = v * u[j];", "const real h = v;"),
     # the first input channel dropped from both dot products
-    "drop_first_term": ("for (int32_t i = 0; i < d; ++i) {\n      const real xi = (real)xb[i];",
-                        "for (int32_t i = 1; i < d; ++i) {\n      const real xi = (real)xb[i];"),
+    "drop_first_term": ("for (int32_t i = 0; i < d; ++i) {\n        const real xi = (real)xb[i];",
+                        "for (int32_t i = 1; i < d; ++i) {\n        const real xi = (real)xb[i];"),
     # W_down read transposed
     "transposed_down": ("s[k] += h * (real)wd_row[k];", "s[k] += h * (real)w_down[(size_t)k * m + j];"),
     # W_gate and W_up swapped
-    "swap_gate_up": ("g[j] += xi * (real)wg_row[j];\n        u[j] += xi * (real)wu_row[j];",
-                     "g[j] += xi * (real)wu_row[j];\n        u[j] += xi * (real)wg_row[j];"),
+    "swap_gate_up": ("g[j] += xi * (real)wg_row[j];\n          u[j] += xi * (real)wu_row[j];",
+                     "g[j] += xi * (real)wu_row[j];\n          u[j] += xi * (real)wg_row[j];"),
     # the dense flag ignored
     "dense_ignored": ("if (!(dense || cats_keeps(v, t))) continue;", "if (!cats_keeps(v, t)) continue;"),
     # residual dropped
