@@ -28,6 +28,11 @@
  *    call returns its status and touches nothing.  HIP failures return
  *    CATS_ERR_HIP.  cats_last_error() gives a message for the last failure
  *    on the calling thread.  No call aborts or throws.
+ *  - Debugging: with the environment variable CATS_SYNC_CHECK set (to
+ *    anything but "" or "0"), every enqueue-only call synchronises `stream`
+ *    after its launches and returns CATS_ERR_HIP for an asynchronous failure
+ *    (a kernel fault, a launch error), naming the call that caused it.  Not
+ *    applied to a stream under graph capture.
  *  - Scratch memory comes from a caller-provided workspace `ws` of
  *    `ws_bytes` bytes (256-byte aligned, device), sized with
  *    cats_workspace_bytes().  Calls that run concurrently need separate

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -33,6 +34,32 @@ cats_status hip_fail(hipError_t e, const char* what) {
 }
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Debug mode: with CATS_SYNC_CHECK set to anything but "" or "0" in the
+// environment, every enqueue-only call synchronises its stream after its
+// launches and reports an asynchronous failure (a kernel fault, a launch
+// error) as CATS_ERR_HIP from the call that launched it.  A stream under
+// graph capture cannot be synchronised; such calls are left as they are.
+bool sync_check_on() {
+  const char* e = std::getenv("CATS_SYNC_CHECK");
+  return e && e[0] && !(e[0] == '0' && e[1] == 0);
+}
+
+cats_status sync_check(void* stream, const char* what) {
+  if (!sync_check_on()) return CATS_OK;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone) return CATS_OK;
+  hipError_t e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, what);
+  e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, what);
+  return CATS_OK;
+}
+
+cats_status checked(cats_status st, void* stream, const char* what) {
+  return st != CATS_OK ? st : sync_check(stream, what);
+}
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -460,7 +487,7 @@ cats_status cats_pack_weights(const void* w, void* w_t, int32_t rows, int32_t co
   if (a < b + bytes && b < a + bytes) return fail(CATS_ERR_RANGE, "w and w_t overlap");
   hipError_t e = cats::launch_transpose(w, w_t, rows, cols, eb, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "transpose launch");
-  return CATS_OK;
+  return sync_check(stream, "cats_pack_weights");
 }
 
 cats_status cats_calib_activations(const cats_layer* layer, const float* x, int32_t N, float* acts,
@@ -473,7 +500,7 @@ cats_status cats_calib_activations(const cats_layer* layer, const float* x, int3
   hipError_t e = cats::launch_calib_acts(layer->wdtype == CATS_BF16, x, layer->w_gate_t, N, layer->d,
                                          layer->m, acts, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "calibration activations launch");
-  return CATS_OK;
+  return sync_check(stream, "cats_calib_activations");
 }
 
 cats_status cats_threshold_from_acts(const float* acts, int64_t n, double sparsity, void* ws,
@@ -521,12 +548,13 @@ cats_status cats_calibrate_threshold(const cats_layer* layer, const float* calib
 cats_status cats_mlp_forward(const cats_layer* layer, const float* x, int32_t B, float t,
                              const float* residual, float* y, const cats_forward_aux* aux, void* ws,
                              size_t ws_bytes, void* stream) {
-  return run_mlp(layer, x, B, t, false, residual, y, aux, ws, ws_bytes, stream);
+  return checked(run_mlp(layer, x, B, t, false, residual, y, aux, ws, ws_bytes, stream), stream, "cats_mlp_forward");
 }
 
 cats_status cats_mlp_dense(const cats_layer* layer, const float* x, int32_t B, const float* residual,
                            float* y, void* ws, size_t ws_bytes, void* stream) {
-  return run_mlp(layer, x, B, 0.f, true, residual, y, nullptr, ws, ws_bytes, stream);
+  return checked(run_mlp(layer, x, B, 0.f, true, residual, y, nullptr, ws, ws_bytes, stream), stream,
+                 "cats_mlp_dense");
 }
 
 cats_status cats_stack_forward(const cats_layer* layers, int32_t L, const float* t, const float* x0,
@@ -580,7 +608,7 @@ cats_status cats_stack_forward(const cats_layer* layers, int32_t L, const float*
     hipError_t e = hipMemcpyAsync(x_out, cur, rows * sizeof(float), hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return hip_fail(e, "x_out copy");
   }
-  return CATS_OK;
+  return sync_check(stream, "cats_stack_forward");
 }
 
 namespace {
@@ -712,7 +740,7 @@ cats_status cats_sparse_input_gemv(const void* w, int32_t d, int32_t n, int32_t 
     e = cats::launch_reduce(ra, s);
     if (e != hipSuccess) return hip_fail(e, "active-list launch");
   }
-  return CATS_OK;
+  return sync_check(stream, "cats_sparse_input_gemv");
 }
 
 namespace {
@@ -840,7 +868,7 @@ cats_status cats_mlp_forward_topk(const cats_layer* layer, const float* x, int32
     e = hipMemcpyAsync(t_out, tbuf, (size_t)B * sizeof(float), hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return hip_fail(e, "cutoff copy");
   }
-  return CATS_OK;
+  return sync_check(stream, "cats_mlp_forward_topk");
 }
 
 size_t cats_unfused_workspace_bytes(int32_t d, int32_t m, int32_t max_batch) {
@@ -920,7 +948,7 @@ cats_status cats_mlp_forward_unfused(const cats_layer* layer, const float* x, in
     e = cats::launch_reduce(ra, s);
     if (e != hipSuccess) return hip_fail(e, "reduce launch");
   }
-  return CATS_OK;
+  return sync_check(stream, "cats_mlp_forward_unfused");
 }
 
 cats_status cats_rmsnorm(const float* x, float* xn, int32_t B, int32_t d, float eps, void* stream) {
@@ -930,7 +958,7 @@ cats_status cats_rmsnorm(const float* x, float* xn, int32_t B, int32_t d, float 
   if (!aligned(x, 4) || !aligned(xn, 4)) return fail(CATS_ERR_ALIGN, "x and xn must be 4-byte aligned");
   hipError_t e = cats::launch_rmsnorm(x, xn, B, d, eps, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "rmsnorm launch");
-  return CATS_OK;
+  return sync_check(stream, "cats_rmsnorm");
 }
 
 cats_status cats_stream_read(const void* buf, size_t bytes, int32_t blocks, int32_t inflight, int32_t runs,
@@ -947,7 +975,7 @@ cats_status cats_stream_read(const void* buf, size_t bytes, int32_t blocks, int3
   hipError_t e = cats::launch_stream_read(buf, (uint32_t)bytes, blocks, inflight, runs != 0, sink,
                                           static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "stream read launch");
-  return CATS_OK;
+  return sync_check(stream, "cats_stream_read");
 }
 
 cats_status cats_timer_enable(int32_t on) {
