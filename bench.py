@@ -558,6 +558,87 @@ def bench_topk(P, W, torch, timed, layers, xs, ks, dense_us, steps, warm):
     return out
 
 
+def profile_set(P, W, torch, layers, xs, thr, ks, calls=6):
+    """Each kernel path of the benchmark run a fixed number of times, for
+    hardware byte counters (rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE).  Returns
+    per path the kernels it launches, the calls and the algorithmic bytes per
+    call (what the path must read and write), which the counters' bytes per
+    dispatch are compared with.  Weight copies rotate as in the timed
+    region; a 256 MiB device copy follows as the counters' scale."""
+    import numpy as np
+
+    dev = xs.device
+    R, ntok = len(layers), xs.shape[0]
+    base = layers[0]
+    d, m = base.d, base.m
+    sw = 2
+    k5 = ks[0]
+    t5 = thr[k5]
+    out = []
+
+    def union(B, t):
+        """Mean |U| over the calls' batches (the union of the rows' active sets)."""
+        us = []
+        for c in range(calls):
+            xb = xs[(c * B) % ntok : (c * B) % ntok + B]
+            _, aux = P.mlp_forward(base, xb, t, aux=True)
+            cnt = aux["cnt"].cpu().numpy()
+            idx = aux["idx"].cpu().numpy()
+            us.append(len(np.unique(np.concatenate([idx[b, : cnt[b]] for b in range(B)]))))
+        return float(np.mean(us))
+
+    def run(label, kernels, fn, bytes_per_call):
+        torch.cuda.synchronize()
+        for c in range(calls):
+            fn(c)
+        torch.cuda.synchronize()
+        out.append({"label": label, "kernels": kernels, "calls": calls, "bytes_per_call": int(bytes_per_call)})
+
+    for B in (1, 4, 8, 16):
+        ws = P.workspace(d, m, B, device=dev)
+        y = torch.empty((B, d), dtype=torch.float32, device=dev)
+        xb = [xs[(c * B) % ntok : (c * B) % ntok + B].contiguous() for c in range(calls)]
+        for k in ((k5,) if B > 1 else ks):
+            U = union(B, thr[k])
+            kern = ["k_mlp_fused", "k_mlp_reduce"] if B <= 4 else ["k_mlp_gateup_mfma", "k_mlp_down_mfma", "k_mlp_reduce"]
+            run(f"forward B={B} k={k}", kern, lambda c, k=k: P.mlp_forward(layers[c % R], xb[c], thr[k], out=y, ws=ws),
+                sw * d * (m + 2 * U) + 8 * B * d)
+        run(f"dense B={B}", ["k_mlp_fused (dense)" if B <= 4 else "k_mlp_gateup_mfma (dense)", "k_mlp_reduce"],
+            lambda c: P.mlp_dense(layers[c % R], xb[c], out=y, ws=ws), 3 * sw * d * m + 8 * B * d)
+        del ws
+    x1 = [xs[c % ntok : c % ntok + 1].contiguous() for c in range(calls)]
+    y1 = torch.empty((1, d), dtype=torch.float32, device=dev)
+    U1 = union(1, t5)
+    run(f"forward with active lists B=1 k={k5}", ["k_mlp_fused (aux)", "k_mlp_reduce (sum and lists)"],
+        lambda c: P.mlp_forward(layers[c % R], x1[c], t5, out=y1, aux=True), sw * d * (m + 2 * U1) + 8 * d + 16 * U1)
+    kept = m - max(1, int(np.ceil(k5 * m - 1e-6))) + 1
+    run(f"top-k B=1 k={k5}", ["k_gate_v", "k_row_select", "k_mlp_fused (given v)", "k_mlp_reduce"],
+        lambda c: P.mlp_forward_topk(layers[c % R], x1[c], k5, out=y1), sw * d * (m + 2 * kept) + 8 * d + 8 * m)
+    for mode in ("mask", "index"):
+        run(f"unfused {mode} B=1 k={k5}", ["k_gate_v", "k_unfused_up", "k_unfused_down", "k_mlp_reduce"],
+            lambda c, mode=mode: P.mlp_forward_unfused(layers[c % R], x1[c], t5, mode=mode, out=y1),
+            sw * d * (m + 2 * U1) + 8 * d + 16 * m)
+    qc = W.CONFIGS["QKV"]
+    wq = W.linear_weight(qc.d, qc.m, qc.wdtype, 5000).to(dev)
+    wqs = [wq] + [wq.clone() for _ in range(R - 1)]
+    xq = W.decode_vectors(qc, calls).to(dev)
+    tq = P.threshold_from_acts(W.calib_vectors(qc).to(dev).reshape(-1).contiguous(), k5)
+    keptq = float(np.mean([int((xq[c].abs() >= tq).sum()) for c in range(calls)]))
+    wsq = P.sparse_input_workspace(qc.d, qc.m, 1, device=dev)
+    yq = torch.empty((1, qc.m), dtype=torch.float32, device=dev)
+    for t, lab, kb in ((tq, f"k={k5}", keptq), (0.0, "dense", qc.d)):
+        run(f"sparse input Q/K/V {lab}", ["k_sparse_input"],
+            lambda c, t=t: P.sparse_input_gemv(wqs[c % R], xq[c : c + 1], t, out=yq, ws=wsq),
+            2 * qc.m * kb + 4 * qc.d + 4 * qc.m)
+    buf = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    sink = torch.empty(1024, dtype=torch.int32, device=dev)
+    run("plain read 256 MiB", ["k_stream_read"], lambda c: P.stream_read(buf, 1024, 8, False, sink), 256 << 20)
+    src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    run("device copy 256 MiB (counter scale)", ["torch copy kernel"], lambda c: dst.copy_(src), 2 * (256 << 20))
+    return out
+
+
 def cpu_baseline(W, cfg, wg, wu, wd, xs, xcal, thr, ks, req_bytes, seconds):
     """The oracle timed on this host (a baseline, never a target): the
     OpenMP build on every core this process may use, and the sequential
@@ -644,6 +725,9 @@ def main() -> int:
     ap.add_argument("--thresholds", default="",
                     help="reload the cutoffs from this thresholds.json (skips calibration)")
     ap.add_argument("--save-thresholds", default="", help="write the cutoffs used to this thresholds.json")
+    ap.add_argument("--profile-set", action="store_true",
+                    help="after the timed region, run each kernel path a fixed number of times "
+                         "(for rocprofv3 byte counters) instead of the extras and the CPU baseline")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="after the timed region, one device-to-device copy of this many MiB "
                          "(a plain copy of known size that scales hardware byte counters)")
@@ -787,6 +871,10 @@ def main() -> int:
         torch.cuda.synchronize()
         out["copy_probe_bytes"] = nb
         del src, dst
+
+    if args.profile_set:
+        out["profile_set"] = profile_set(P, W, torch, layers, xs, thr, ks)
+        args.no_extras = args.no_stacks = args.no_cpu_baseline = True
 
     if not args.no_extras:
         per_k = {}
