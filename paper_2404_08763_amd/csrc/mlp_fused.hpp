@@ -135,6 +135,46 @@ __global__ __launch_bounds__(fused_waves(NCH, BT, VIN)* kWaveSize) void k_mlp_fu
     for (int b = 0; b < BT; ++b) out[b] = (b < B) ? wave_sum(acc[b]) * xscale[b] : 0.f;
   };
 
+  // Dot products of two weight rows (a gate row and the previous neuron's
+  // up row) with the staged x rows in one pass, so each x value is read
+  // from LDS once for both; each accumulator sums in row_dot's order, so the
+  // results are row_dot's bits.
+  auto row_dot2 = [&](const u32x4(&bufa)[NCH], const u32x4(&bufb)[NCH], float(&outa)[BT], float(&outb)[BT]) {
+    float acca[BT], accb[BT];
+#pragma unroll
+    for (int b = 0; b < BT; ++b) acca[b] = accb[b] = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int col = c * CH + lane * VEC;
+      float wa[VEC], wb[VEC];
+      widen<WT>(bufa[c], wa);
+      widen<WT>(bufb[c], wb);
+#pragma unroll
+      for (int b = 0; b < BT; ++b) {
+        if (b < B) {
+          const float* xp = xs + b * DP + col;
+#pragma unroll
+          for (int e4 = 0; e4 < VEC; e4 += 4) {
+            const f32x4 xv = *reinterpret_cast<const f32x4*>(xp + e4);
+            acca[b] = fmaf(wa[e4 + 0], xv.x, acca[b]);
+            acca[b] = fmaf(wa[e4 + 1], xv.y, acca[b]);
+            acca[b] = fmaf(wa[e4 + 2], xv.z, acca[b]);
+            acca[b] = fmaf(wa[e4 + 3], xv.w, acca[b]);
+            accb[b] = fmaf(wb[e4 + 0], xv.x, accb[b]);
+            accb[b] = fmaf(wb[e4 + 1], xv.y, accb[b]);
+            accb[b] = fmaf(wb[e4 + 2], xv.z, accb[b]);
+            accb[b] = fmaf(wb[e4 + 3], xv.w, accb[b]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < BT; ++b) {
+      outa[b] = (b < B) ? wave_sum(acca[b]) * xscale[b] : 0.f;
+      outb[b] = (b < B) ? wave_sum(accb[b]) * xscale[b] : 0.f;
+    }
+  };
+
   // ---- stage x (rows past B and columns past d read as zero); its loads
   // go out first so the first gate row can stay in flight while x is
   // written to LDS
@@ -195,21 +235,36 @@ __global__ __launch_bounds__(fused_waves(NCH, BT, VIN)* kWaveSize) void k_mlp_fu
 #pragma unroll
   for (int b = 0; b < BT; ++b) pv[b] = 0.f;
 
+  // With several rows (and the gate computed here) the gate dot of neuron
+  // i and the up dot of neuron i - 1 share one pass over x: at 2..8 rows the
+  // LDS reads of the staged rows, not the weight stream, set the pace.
+  constexpr bool kPaired = BT > 1 && !VIN;
   // iteration i: prefetch gate(i+1) into gnxt; gate(i) -> mask, issue
   // up(i); finish up(i-1).
   auto iter = [&](int i, u32x4(&gcur)[NCH], u32x4(&gnxt)[NCH], u32x4(&ucur)[NCH],
                   u32x4(&uprev)[NCH]) {
     if constexpr (!VIN) load_row(gnxt, rg, row_base(i + 1 < ni, n0 + w + (i + 1) * W));
     uint32_t mask = 0;
-    float v[BT];
+    float v[BT], up2[BT];
 #pragma unroll
     for (int b = 0; b < BT; ++b) v[b] = 0.f;
+    if constexpr (kPaired) {
+      // both buffers are consumed on every path (a missing neuron's rows read
+      // as zeros), which keeps the count of loads in flight exact
+      float g[BT];
+      row_dot2(gcur, uprev, g, up2);
+      if (i < ni) {
+#pragma unroll
+        for (int b = 0; b < BT; ++b)
+          if (b < B) v[b] = silu(g[b]);
+      }
+    }
     if (i < ni) {
       if constexpr (VIN) {
 #pragma unroll
         for (int b = 0; b < BT; ++b)
           if (b < B) v[b] = l_v[w + i * W][b];
-      } else {
+      } else if constexpr (!kPaired) {
         float g[BT];
         row_dot(gcur, g);
 #pragma unroll
@@ -233,7 +288,10 @@ __global__ __launch_bounds__(fused_waves(NCH, BT, VIN)* kWaveSize) void k_mlp_fu
       // the zeros; with one row (the mask is then wave-uniform) a masked
       // neuron only waits for its dataless load and skips the dot.
       float h[BT], u[BT];
-      if (BT == 1 && uniform_u32(pmask) == 0u) {
+      if constexpr (kPaired) {
+#pragma unroll
+        for (int b = 0; b < BT; ++b) u[b] = up2[b];
+      } else if (BT == 1 && uniform_u32(pmask) == 0u) {
 #pragma unroll
         for (int c = 0; c < NCH; ++c) asm volatile("" ::"v"(uprev[c]));
 #pragma unroll
