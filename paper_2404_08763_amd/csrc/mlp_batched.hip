@@ -62,11 +62,20 @@ __device__ __forceinline__ void split8(const u32x4& a, const u32x4& b, bf16x8& h
   lo = as_bf16x8(lv);
 }
 
+// Weight steps a wave keeps in flight: a whole tile up to eight steps; at
+// ten (d = 5120) the x slice takes 80 registers and a whole tile 40 more,
+// past the 128 a wave has at four waves per SIMD, so the loads run two
+// steps ahead instead (five still spill).
+template <int KS>
+constexpr int gateup_window() { return KS <= 8 ? KS : 2; }
+
 // KS: MFMA k-steps (32 columns each) per wave; the kernel covers
 // d = kGW * 32 * KS columns exactly, so no column needs a bounds check.
 template <int KS, bool DENSE, bool AUX>
 __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
   constexpr int KW = 32 * KS;  // columns per wave
+  constexpr int WIN = gateup_window<KS>();
+  static_assert(KS % WIN == 0, "a tile's steps must fill the window evenly");
   constexpr int NBMAX = kFusedMaxNeurons;
 
   __shared__ f32x4 red[kGW * kWaveSize];        // the waves' partial tiles
@@ -162,11 +171,14 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
   // The first gate tile's weights go out only now: issued before the x
   // fragments are built, they would sit in registers the fragments need,
   // and the compiler parks them elsewhere one load round trip at a time.
-  u32x4 buf[KS];
+  // buf[s % WIN] holds step s of the current tile; the loads stream over
+  // (tile, step) pairs WIN steps ahead of the products, into the next tile
+  // once the current one's steps are all out.
+  u32x4 buf[WIN];
+  uint32_t rbc = row_of(0);  // row base of the current operation
   {
-    const uint32_t rb = row_of(0);
 #pragma unroll
-    for (int s = 0; s < KS; ++s) buf[s] = ld_buf16_stream(rg, rb + colb + s * 64u);
+    for (int s = 0; s < WIN; ++s) buf[s] = ld_buf16_stream(rg, rbc + colb + s * 64u);
   }
   __syncthreads();
 
@@ -175,7 +187,14 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
     // tile i is reduced; with a single tile that is after this operation.
     const bool defer = (T == 1 && op == 0);
     const uint32_t rbn = defer ? kOOB : row_of(op + 1);
+    const __amdgpu_buffer_rsrc_t rc = op < T ? rg : ru;
     const __amdgpu_buffer_rsrc_t rn = (op + 1 < T) ? rg : ru;
+    // the load WIN steps after step f - WIN: step f of this tile, or step
+    // f - KS of the next
+    auto ld_ahead = [&](int f) -> u32x4 {
+      return f < KS ? ld_buf16_stream(rc, rbc + colb + f * 64u)
+                    : ld_buf16_stream(rn, rbn + colb + (f - KS) * 64u);
+    };
     // Four independent accumulators (hi and lo products of even and odd
     // steps) keep the matrix core pipelined instead of waiting on one chain;
     // they are added in a fixed order at the end.  A step's buffer is
@@ -183,7 +202,7 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
     f32x4 ah0 = {0.f, 0.f, 0.f, 0.f}, ah1 = ah0, al0 = ah0, al1 = ah0;
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      const bf16x8 av = as_bf16x8(buf[s]);
+      const bf16x8 av = as_bf16x8(buf[s % WIN]);
       if (s & 1) {
         ah1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, xh[s], ah1, 0, 0, 0);
         al1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, xl[s], al1, 0, 0, 0);
@@ -191,10 +210,11 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
         ah0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, xh[s], ah0, 0, 0, 0);
         al0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, xl[s], al0, 0, 0, 0);
       }
-      if (s >= 1) buf[s - 1] = ld_buf16_stream(rn, rbn + colb + (s - 1) * 64u);
+      if (s >= 1) buf[(s - 1) % WIN] = ld_ahead(s - 1 + WIN);
       __builtin_amdgcn_sched_barrier(0);
     }
-    buf[KS - 1] = ld_buf16_stream(rn, rbn + colb + (KS - 1) * 64u);
+    buf[(KS - 1) % WIN] = ld_ahead(KS - 1 + WIN);
+    rbc = rbn;
     const f32x4 acc = (ah0 + ah1) + (al0 + al1);
     red[w * kWaveSize + lane] = acc;
     __syncthreads();
@@ -220,9 +240,9 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
     }
     __syncthreads();
     if (defer) {
-      const uint32_t rb = row_of(1);
+      rbc = row_of(1);
 #pragma unroll
-      for (int s = 0; s < KS; ++s) buf[s] = ld_buf16_stream(ru, rb + colb + s * 64u);
+      for (int s = 0; s < WIN; ++s) buf[s] = ld_buf16_stream(ru, rbc + colb + s * 64u);
     }
   }
 
@@ -461,6 +481,7 @@ static hipError_t launch_gateup_t(int ks, const BatchedArgs& a, int G, hipStream
     CATS_KS(4)
     CATS_KS(6)
     CATS_KS(8)
+    CATS_KS(10)
 #undef CATS_KS
     default: return hipErrorInvalidValue;
   }
@@ -471,7 +492,7 @@ int batched_ks(int d) {
   if (d % (kGW * 32) != 0) return 0;
   const int ks = d / (kGW * 32);
   // instantiated widths; wider rows do not fit the register-resident x slice
-  return (ks == 1 || ks == 2 || ks == 4 || ks == 6 || ks == 8) ? ks : 0;
+  return (ks == 1 || ks == 2 || ks == 4 || ks == 6 || ks == 8 || ks == 10) ? ks : 0;
 }
 
 hipError_t launch_gateup(bool dense, bool aux, const BatchedArgs& a, int G, hipStream_t s) {

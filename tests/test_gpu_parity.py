@@ -178,9 +178,9 @@ def test_batch_rows_have_their_own_masks(dev, oracle32, B):
 
 
 # ------------------------------------------------ batched (matrix-core) path
-# bf16 weights, 5..16 rows and d of 512, 1024, 2048, 3072 or 4096
+# bf16 weights, 5..16 rows and d of 512, 1024, 2048, 3072, 4096 or 5120
 @pytest.mark.parametrize("d,m,B", [(512, 7, 5), (512, 300, 8), (1024, 693, 16), (1024, 693, 6), (3072, 500, 7),
-                                   (4096, 1100, 16), (2048, 4111, 12)])
+                                   (4096, 1100, 16), (2048, 4111, 12), (5120, 700, 16), (5120, 2063, 5)])
 def test_batched_path_vs_oracle(dev, oracle32, d, m, B):
     c = W.shrink(W.CONFIGS["C3"], d, m)
     wg, wu, wd = W.weights(d, m, torch.bfloat16, layer=6)
@@ -209,9 +209,11 @@ def test_batched_path_vs_oracle(dev, oracle32, d, m, B):
     assert torch.equal(yi.cpu(), res)
 
 
-def test_batched_full_size_c2(dev, oracle32):
-    """Llama2-7B-shaped block at 16 rows (the batched path), k = 0.5 and 0.7."""
-    c = W.CONFIGS["C2"]
+@pytest.mark.parametrize("name", ["C2", "C4"])
+def test_batched_full_size(dev, oracle32, name):
+    """Llama2-7B- and Llama2-13B-shaped blocks at 16 rows (the batched
+    path), k = 0.5 and 0.7."""
+    c = W.CONFIGS[name]
     wg, wu, wd = W.weights(c.d, c.m, c.wdtype)
     layer = device_layer(wg, wu, wd)
     hw = host_f32(wg, wu, wd)
@@ -221,12 +223,12 @@ def test_batched_full_size_c2(dev, oracle32):
     ws = P.workspace(c.d, c.m, B)
     for k in (0.5, 0.7):
         t = quantile_t(np.abs(ref_all["v"]), k)
-        say("C2 batched B16 k", k, "t", t)
+        say(name, "batched B16 k", k, "t", t)
         y, aux = P.mlp_forward(layer, x.cuda(), t, ws=ws, aux=True)
         ref = oracle32.cats_mlp(x.numpy(), *hw, t=t)
-        r = check_forward(y, aux, ref, t, B, f"C2 B16 k{k}", ref_all=ref_all, w_down=hw[2],
+        r = check_forward(y, aux, ref, t, B, f"{name} B16 k{k}", ref_all=ref_all, w_down=hw[2],
                           h_abs=h_bound(x.numpy(), hw[1], ref_all["v"]))
-        print(f"[batched] C2 B16 k{k}: y err {r['y_err']:.3e} (reconciled {r['y_err_reconciled']:.3e}) "
+        print(f"[batched] {name} B16 k{k}: y err {r['y_err']:.3e} (reconciled {r['y_err_reconciled']:.3e}) "
               f"of {r['y_scale']:.3e}, {r['band_flips']} band flips")
         y2 = P.mlp_forward(layer, x.cuda(), t, ws=ws)
         assert torch.equal(y.view(torch.int32), y2.view(torch.int32))
