@@ -17,12 +17,12 @@
 // column tile leave
 // device-coherent partial sums and take a ticket; the last of them adds the
 // NG partials in group order (deterministic), adds the residual and writes
-// y.  No block waits for another: the ticket is a compare-and-swap on a
-// word tagged with this call's epoch, so leftovers of earlier calls in the
-// workspace are simply restarted, and the loop only repeats when another
-// block's swap succeeded (at most NG times).  The last block puts the count
-// back to zero under the same tag, so a replayed graph, which repeats the
-// epoch it was captured with, finds its tickets fresh too.
+// y.  No block waits for another.  The ticket is a count in a word tagged
+// with the call's epoch: one atomic add when the word already carries this
+// call's tag, else a compare-and-swap that restarts the count under it, so
+// leftovers of earlier calls in the workspace never count (the swap loop
+// only repeats when another block's swap succeeded, at most NG times).  The
+// last block leaves the count at zero under the next epoch's tag.
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -243,19 +243,34 @@ __global__ __launch_bounds__(kSThreads) void k_sparse_input(SparseInputArgs a) {
   __syncthreads();
   if (tid == 0) {
     unsigned long long* tk = a.tickets + ct;
-    unsigned long long old = __hip_atomic_load(tk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    unsigned long long want;
-    for (;;) {
-      want = ((old >> 32) == (unsigned long long)a.epoch) ? old + 1ull : (((unsigned long long)a.epoch << 32) | 1ull);
-      if (__hip_atomic_compare_exchange_strong(tk, &old, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT))
-        break;
+    const unsigned long long tag = (unsigned long long)a.epoch << 32;
+    // Fast path: the word already carries this call's tag (the previous
+    // call on this workspace left it so), and one atomic add counts the
+    // block.  Otherwise the word is stale: compare-and-swap until this
+    // call's tag is installed or counted on (an add that landed on the
+    // stale word is overwritten by the install, so it is not counted).
+    unsigned long long old = __hip_atomic_fetch_add(tk, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    unsigned long long want = old + 1ull;
+    if ((old >> 32) != (unsigned long long)a.epoch) {
+      old = __hip_atomic_load(tk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (;;) {
+        want = ((old >> 32) == (unsigned long long)a.epoch) ? old + 1ull : (tag | 1ull);
+        if (__hip_atomic_compare_exchange_strong(tk, &old, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT))
+          break;
+      }
     }
     s_last = (int)(want & 0xffffffffull) == NG;
-    // The tile's count is complete: return it to zero under the same tag,
-    // so a call that repeats this epoch (a replayed graph) starts afresh.
-    if (s_last)
-      __hip_atomic_store(tk, (unsigned long long)a.epoch << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // The tile's count is complete: leave it at zero under the tag that
+    // the next call carries when it directly follows this one (epochs
+    // count up and skip 0), so that call takes the fast path.  Any other
+    // next call (another workspace's call in between, or a replayed graph,
+    // which repeats its captured epoch) finds a stale tag and takes the
+    // compare-and-swap path, which is also exact.
+    if (s_last) {
+      const uint32_t next = a.epoch == 0xffffffffu ? 1u : a.epoch + 1u;
+      __hip_atomic_store(tk, (unsigned long long)next << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
   __syncthreads();
   if (!s_last || !item) return;

@@ -66,7 +66,11 @@ def test_qkv_full_size(dev, oracle32):
     _check(oracle32, w, x, t, res=res, label="QKV B16")
 
 
-@pytest.mark.parametrize("d,n,B", [(1000, 1504, 3), (7, 8, 1), (4096, 1024, 8), (333, 2056, 16)])
+# Ragged and wide shapes: one to many channel groups and column tiles
+# (n up to 16384), and (16384, 2048, 1) with four compaction rounds.
+@pytest.mark.parametrize("d,n,B", [(1000, 1504, 3), (7, 8, 1), (4096, 1024, 8), (333, 2056, 16),
+                                   (4096, 4096, 2), (2048, 11008, 1), (1024, 14336, 3), (4096, 16384, 4),
+                                   (3000, 10240, 4), (16384, 2048, 1), (5000, 3000, 4), (64, 16384, 2)])
 def test_ragged_and_edges(dev, oracle32, d, n, B):
     w = W.linear_weight(d, n, torch.bfloat16, SEED_W + d)
     x = torch.randn((B, d), generator=torch.Generator().manual_seed(d + n))
