@@ -321,6 +321,15 @@ def bench_sparse_input(P, W, torch, timed, steps, warm, rotate):
     timed(lambda s: call(s, thr[0.5]), 0, 32)
     P.timer_enable(False)
     out["kernel_avg_us_k0.5"] = {nme: round(v[1] * 1e3 / max(1, v[0]), 3) for nme, v in P.timer_read().items() if v[0]}
+    # the same bytes as one plain read launch (best of the stream-read sweep,
+    # start and tail included): what a single pass over them costs
+    plain = {}
+    for name, nbytes, us in (("0.5", 2 * n * int(round(kept[0.5].mean())), out["0.5"]["us"]),
+                             ("dense", 2 * d * n, out["dense_us"])):
+        one = bench_attainable(P, torch, dev, nbytes)["one_launch"]
+        plain[name] = {"bytes": nbytes, "plain_read_us": one["us"], "plain_read_gbps": one["gbps"],
+                       "ratio_to_plain_read": round(us / one["us"], 3)}
+    out["vs_one_launch_plain_read"] = plain
     return out
 
 
@@ -618,6 +627,29 @@ def profile_set(P, W, torch, layers, xs, thr, ks, calls=6):
         run(f"unfused {mode} B=1 k={k5}", ["k_gate_v", "k_unfused_up", "k_unfused_down", "k_mlp_reduce"],
             lambda c, mode=mode: P.mlp_forward_unfused(layers[c % R], x1[c], t5, mode=mode, out=y1),
             sw * d * (m + 2 * U1) + 8 * d + 16 * m)
+    # the Llama2-13B-shaped block at 16 rows: the matrix-core path at
+    # d = 5120 (ten k-steps per wave)
+    c4 = W.CONFIGS["C4"]
+    g4, u4, d4 = W.weights(c4.d, c4.m, c4.wdtype)
+    l4 = P.layer_from_math(g4.to(dev), u4.to(dev), d4.to(dev))
+    del g4, u4, d4
+    l4s = [l4, P.Layer(l4.w_gate_t.clone(), l4.w_up_t.clone(), l4.w_down.clone())]
+    x4 = W.decode_vectors(c4, calls * 16).to(dev)
+    ws4 = P.workspace(c4.d, c4.m, 16, 256 * c4.m, device=dev)
+    t4 = P.calibrate_threshold(l4, W.calib_vectors(c4, 256).to(dev), k5, ws=ws4)
+    xb4 = [x4[c * 16 : (c + 1) * 16].contiguous() for c in range(calls)]
+    y4 = torch.empty((16, c4.d), dtype=torch.float32, device=dev)
+    U4 = []
+    for c in range(calls):
+        _, a4 = P.mlp_forward(l4, xb4[c], t4, aux=True, ws=ws4)
+        cnt, idx = a4["cnt"].cpu().numpy(), a4["idx"].cpu().numpy()
+        U4.append(len(np.unique(np.concatenate([idx[b, : cnt[b]] for b in range(16)]))))
+    run(f"13B-shaped forward B=16 k={k5}", ["k_mlp_gateup_mfma", "k_mlp_down_mfma", "k_mlp_reduce"],
+        lambda c: P.mlp_forward(l4s[c % 2], xb4[c], t4, out=y4, ws=ws4),
+        sw * c4.d * (c4.m + 2 * float(np.mean(U4))) + 8 * 16 * c4.d)
+    run("13B-shaped dense B=16", ["k_mlp_gateup_mfma (dense)", "k_mlp_down_mfma", "k_mlp_reduce"],
+        lambda c: P.mlp_dense(l4s[c % 2], xb4[c], out=y4, ws=ws4), 3 * sw * c4.d * c4.m + 8 * 16 * c4.d)
+    del l4s, l4, ws4
     qc = W.CONFIGS["QKV"]
     wq = W.linear_weight(qc.d, qc.m, qc.wdtype, 5000).to(dev)
     wqs = [wq] + [wq.clone() for _ in range(R - 1)]
