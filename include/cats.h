@@ -224,8 +224,9 @@ cats_status cats_stack_forward(const cats_layer* layers, int32_t L, const float*
  * r = ceil(sparsity * m - 1e-6) clamped to [1, m] (Eq. 3 over one token);
  * sparsity = 0 keeps every neuron.  Each row keeps at least m - r + 1
  * neurons (ties at t_b are kept).  Three steps on `stream`: the gate
- * activations of all rows, an exact per-row radix select, and the fused
- * forward reading those activations (W_gate is read once).  Arguments as
+ * activations of all rows, an exact per-row radix select (for a single row
+ * of up to 16384 neurons done by the gate kernel's last block), and the
+ * fused forward reading those activations (W_gate is read once).  Arguments as
  * cats_mlp_forward; t_out: dev [B] fp32 receiving t_b, or NULL.  Rows are
  * processed in passes of at most 8 (the vector-ALU kernel).  Workspace:
  * cats_topk_workspace_bytes(d, m, B).  Enqueue only. */

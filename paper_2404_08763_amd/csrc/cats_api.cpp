@@ -815,11 +815,13 @@ cats_status cats_calibrate_stack(const cats_layer* layers, int32_t L, const floa
   return CATS_OK;
 }
 
+// Top-k workspace: the forward's, then v [B x m], the cutoffs [B] and the
+// gate blocks' arrival count of the in-kernel select (one 64-bit word).
 size_t cats_topk_workspace_bytes(int32_t d, int32_t m, int32_t max_batch) {
   const size_t base = round_up(cats_workspace_bytes(d, m, max_batch, 0), kAlign);
   if (base == 0) return 0;
   return base + round_up((size_t)max_batch * m * sizeof(float), kAlign) +
-         round_up((size_t)max_batch * sizeof(float), kAlign);
+         round_up((size_t)max_batch * sizeof(float), kAlign) + kAlign;
 }
 
 cats_status cats_mlp_forward_topk(const cats_layer* layer, const float* x, int32_t B, double sparsity,
@@ -844,24 +846,49 @@ cats_status cats_mlp_forward_topk(const cats_layer* layer, const float* x, int32
   if (st != CATS_OK) return st;
   float* vbuf = reinterpret_cast<float*>(static_cast<char*>(ws) + base);
   float* tbuf = reinterpret_cast<float*>(static_cast<char*>(ws) + base + round_up((size_t)B * m * sizeof(float), kAlign));
+  unsigned long long* ticket = reinterpret_cast<unsigned long long*>(
+      reinterpret_cast<char*>(tbuf) + round_up((size_t)B * sizeof(float), kAlign));
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const int nch = cats::fused_nch(bf16, d);
   const int bt_max = cats::fused_bt_max(bf16, nch);
   const int G = cats::fused_grid(m);
-  for (int b0 = 0; b0 < B; b0 += bt_max) {
-    const int bp = (B - b0) < bt_max ? (B - b0) : bt_max;
+  const int64_t rank = cutoff_rank(m, sparsity);
+  // One row of up to kGateSelMaxM neurons: the gate kernel's last block
+  // selects the cutoff itself (no select launch).
+  const bool sel_in_gate = B == 1 && m <= cats::kGateSelMaxM;
+  if (sel_in_gate) {
     cats::GateVArgs ga{};
     ga.wg = layer->w_gate_t;
-    ga.x = x + (size_t)b0 * d;
-    ga.B = bp;
+    ga.x = x;
+    ga.B = 1;
     ga.d = d;
     ga.m = m;
-    ga.v = vbuf + (size_t)b0 * m;
-    hipError_t e = cats::launch_gate_v(bf16, nch, batch_tile(bp), false, ga, G, s);
-    if (e != hipSuccess) return hip_fail(e, "gate activation launch");
+    ga.v = vbuf;
+    ga.rank = (int)rank;
+    ga.t_out = tbuf;
+    ga.ticket = ticket;
+    ga.epoch = next_epoch();
+    hipError_t e = cats::launch_gate_v_select(bf16, nch, ga, G, s);
+    if (e != hipSuccess) return hip_fail(e, "gate activation and cutoff launch");
+  } else {
+    for (int b0 = 0; b0 < B; b0 += bt_max) {
+      const int bp = (B - b0) < bt_max ? (B - b0) : bt_max;
+      cats::GateVArgs ga{};
+      ga.wg = layer->w_gate_t;
+      ga.x = x + (size_t)b0 * d;
+      ga.B = bp;
+      ga.d = d;
+      ga.m = m;
+      ga.v = vbuf + (size_t)b0 * m;
+      hipError_t e = cats::launch_gate_v(bf16, nch, batch_tile(bp), false, ga, G, s);
+      if (e != hipSuccess) return hip_fail(e, "gate activation launch");
+    }
   }
-  hipError_t e = cats::launch_row_select(vbuf, B, m, cutoff_rank(m, sparsity), tbuf, s);
-  if (e != hipSuccess) return hip_fail(e, "per-row cutoff launch");
+  hipError_t e = hipSuccess;
+  if (!sel_in_gate) {
+    e = cats::launch_row_select(vbuf, B, m, rank, tbuf, s);
+    if (e != hipSuccess) return hip_fail(e, "per-row cutoff launch");
+  }
   st = run_mlp(layer, x, B, 0.f, false, residual, y, aux, ws, base, stream, false, 0.f, vbuf, tbuf);
   if (st != CATS_OK) return st;
   if (t_out) {

@@ -9,18 +9,31 @@
 //
 // A block owns the fused kernel's neuron range; wave w walks neurons
 // n0 + w, n0 + w + W, ... with the next row in flight while one is reduced.
+//
+// With SEL (one row, m up to kGateSelMaxM) the kernel also fixes the row's
+// top-k cutoff: every block writes its v with device-coherent stores and
+// takes a ticket (the sparse-input kernel's epoch-tagged count: one atomic
+// add when the word carries this call's tag, a compare-and-swap restart on
+// a stale one); the last block to arrive reads the whole row back and
+// selects its r-th smallest |v| (topk_select.hpp), so no separate select
+// launch is needed.  No block waits for another.
 #include "gemv_rows.hpp"
+#include "topk_select.hpp"
 
 namespace cats {
 
-template <typename WT, int NCH, int BT, bool SEG>
+template <typename WT, int NCH, int BT, bool SEG, bool SEL>
 __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_gate_v(GateVArgs a) {
   typedef RowGeom<WT, NCH> R;
   constexpr int W = kFusedWaves;
   constexpr int NT = W * kWaveSize;
+  static_assert(!SEL || (BT == 1 && !SEG), "the in-kernel select takes one row");
   __shared__ __attribute__((aligned(16))) float xs[BT * R::DP];
   __shared__ uint32_t l_mask[SEG ? kFusedMaxNeurons : 1];
   __shared__ int w_cnt[W + 1];
+  __shared__ __attribute__((aligned(16))) uint32_t hist[SEL ? kSelHistBins : 1];
+  __shared__ uint32_t s_state[4];
+  __shared__ int s_last;
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWaveSize - 1);
@@ -48,7 +61,12 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_gate_v(GateVArgs a) 
     for (int b = 0; b < BT; ++b) {
       if (b < B) {
         const float v = silu(g[b]);
-        if (lane == 0 && i < ni) a.v[(size_t)b * m + j] = v;
+        if (lane == 0 && i < ni) {
+          if constexpr (SEL)
+            __hip_atomic_store(a.v + j, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          else
+            a.v[(size_t)b * m + j] = v;
+        }
         mask |= (uint32_t)!(fabsf(v) < a.t) << b;
       }
     }
@@ -65,6 +83,49 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_gate_v(GateVArgs a) 
     const int cnt = compact_block<W>(l_mask, nr.nb, nr.n0, a.seg_j, a.seg_mask, w_cnt);
     if (tid == 0) a.seg_cnt[blockIdx.x] = cnt;
   }
+  if constexpr (SEL) {
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's v stores have completed
+    __syncthreads();
+    if (tid == 0) {
+      const unsigned long long tag = (unsigned long long)a.epoch << 32;
+      unsigned long long old = __hip_atomic_fetch_add(a.ticket, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      unsigned long long want = old + 1ull;
+      if ((old >> 32) != (unsigned long long)a.epoch) {
+        old = __hip_atomic_load(a.ticket, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (;;) {
+          want = ((old >> 32) == (unsigned long long)a.epoch) ? old + 1ull : (tag | 1ull);
+          if (__hip_atomic_compare_exchange_strong(a.ticket, &old, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT))
+            break;
+        }
+      }
+      s_last = (int)(want & 0xffffffffull) == (int)gridDim.x;
+      if (s_last) {
+        const uint32_t next = a.epoch == 0xffffffffu ? 1u : a.epoch + 1u;
+        __hip_atomic_store(a.ticket, (unsigned long long)next << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    __syncthreads();
+    if (!s_last) return;
+    // the last block: every block's v is in memory
+    if (a.rank <= 0) {
+      if (tid == 0) a.t_out[0] = 0.f;
+      return;
+    }
+    // device-coherent loads, all in flight at once (out of range past m)
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(a.v, (uint32_t)m * 4u);
+    uint32_t key[kGateSelKeys];
+#pragma unroll
+    for (int k = 0; k < kGateSelKeys; ++k) {
+      const int i = tid + k * NT;
+      key[k] = __builtin_amdgcn_raw_buffer_load_b32(rv, i < m ? (int)((uint32_t)i * 4u) : (int)kOOB, 0, kCachePolicySc1);
+    }
+#pragma unroll
+    for (int k = 0; k < kGateSelKeys; ++k)
+      key[k] = tid + k * NT < m ? (key[k] & 0x7fffffffu) : 0xffffffffu;  // |v| as bits; padding never matches
+    const float tb = select_rank<NT, kGateSelKeys>(key, a.rank, hist, s_state);
+    if (tid == 0) a.t_out[0] = tb;
+  }
 }
 
 template <typename WT, int NCH, bool SEG>
@@ -73,17 +134,17 @@ static hipError_t launch_gate_v_nch(int bt, const GateVArgs& a, int G, hipStream
   const dim3 grid(G), block(kFusedWaves * kWaveSize);
   KernelTimer timer(SEG ? "gate_v_list" : "gate_v", s);
   switch (bt) {
-    case 1: hipExtLaunchKernelGGL((k_gate_v<WT, NCH, 1, SEG>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
-    case 2: hipExtLaunchKernelGGL((k_gate_v<WT, NCH, 2, SEG>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
+    case 1: hipExtLaunchKernelGGL((k_gate_v<WT, NCH, 1, SEG, false>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
+    case 2: hipExtLaunchKernelGGL((k_gate_v<WT, NCH, 2, SEG, false>), grid, block, 0, s, timer.start(), timer.stop(), 0, a); break;
     case 4:
       if constexpr (4 * DP * 4 <= kXLdsBytes) {
-        hipExtLaunchKernelGGL((k_gate_v<WT, NCH, 4, SEG>), grid, block, 0, s, timer.start(), timer.stop(), 0, a);
+        hipExtLaunchKernelGGL((k_gate_v<WT, NCH, 4, SEG, false>), grid, block, 0, s, timer.start(), timer.stop(), 0, a);
         break;
       }
       return hipErrorInvalidValue;
     case 8:
       if constexpr (8 * DP * 4 <= kXLdsBytes) {
-        hipExtLaunchKernelGGL((k_gate_v<WT, NCH, 8, SEG>), grid, block, 0, s, timer.start(), timer.stop(), 0, a);
+        hipExtLaunchKernelGGL((k_gate_v<WT, NCH, 8, SEG, false>), grid, block, 0, s, timer.start(), timer.stop(), 0, a);
         break;
       }
       return hipErrorInvalidValue;
@@ -103,6 +164,33 @@ static hipError_t launch_gate_v_t(int nch, int bt, const GateVArgs& a, int G, hi
     case 16: return launch_gate_v_nch<WT, 16, SEG>(bt, a, G, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+template <typename WT>
+static hipError_t launch_gate_v_sel_t(int nch, const GateVArgs& a, int G, hipStream_t s) {
+  const dim3 grid(G), block(kFusedWaves * kWaveSize);
+  KernelTimer timer("gate_v_select", s);
+  switch (nch) {
+#define CATS_SEL(N)                                                                                  \
+  case N:                                                                                            \
+    hipExtLaunchKernelGGL((k_gate_v<WT, N, 1, false, true>), grid, block, 0, s, timer.start(),        \
+                          timer.stop(), 0, a);                                                       \
+    break;
+    CATS_SEL(1)
+    CATS_SEL(2)
+    CATS_SEL(4)
+    CATS_SEL(8)
+    CATS_SEL(10)
+    CATS_SEL(16)
+#undef CATS_SEL
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_v_select(int wdtype_bf16, int nch, const GateVArgs& a, int G, hipStream_t s) {
+  if (a.B != 1 || a.m > kGateSelMaxM) return hipErrorInvalidValue;
+  return wdtype_bf16 ? launch_gate_v_sel_t<wbf16>(nch, a, G, s) : launch_gate_v_sel_t<wf32>(nch, a, G, s);
 }
 
 hipError_t launch_gate_v(int wdtype_bf16, int nch, int bt, bool seg, const GateVArgs& a, int G, hipStream_t s) {

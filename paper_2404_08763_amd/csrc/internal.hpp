@@ -131,8 +131,19 @@ struct GateVArgs {
   int* seg_j;          // with the list: [m] per block, its active neurons ascending
   uint32_t* seg_mask;  // [m] their row masks
   int* seg_cnt;        // [G]
+  // with the in-kernel select (one row): the cutoff rank r (0 gives t = 0),
+  // where t goes, and the epoch-tagged arrival count of the blocks
+  int rank;
+  float* t_out;
+  unsigned long long* ticket;
+  uint32_t epoch;
 };
+// The in-kernel select holds the row's keys in registers: kGateSelKeys per
+// thread of a gate block, so rows of up to kGateSelMaxM neurons.
+constexpr int kGateSelKeys = 32;
+constexpr int kGateSelMaxM = kGateSelKeys * kFusedWaves * 64;  // 64-lane waves
 hipError_t launch_gate_v(int wdtype_bf16, int nch, int bt, bool seg, const GateVArgs& a, int G, hipStream_t s);
+hipError_t launch_gate_v_select(int wdtype_bf16, int nch, const GateVArgs& a, int G, hipStream_t s);
 hipError_t launch_row_select(const float* v, int B, int m, int64_t r, float* t, hipStream_t s);
 hipError_t launch_fused_bf16_topk(int nch, int bt, bool aux, const FusedArgs& a, int G, hipStream_t s);
 hipError_t launch_fused_f32_topk(int nch, int bt, bool aux, const FusedArgs& a, int G, hipStream_t s);
