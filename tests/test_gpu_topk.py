@@ -104,6 +104,19 @@ def test_topk_small_bf16(small_bf16, oracle32, B, k):
     _check(oracle32, layer, hw, _x(B, 1032), k, f"small bf16 B{B} k{k}")
 
 
+# One row selects inside the gate kernel up to 16384 neurons (32 keys per
+# thread of a 512-thread block) and in the separate select kernel beyond:
+# both sides of the limit, and a width with a single neuron per block.
+@pytest.mark.parametrize("m", [16384, 16392, 257])
+def test_topk_select_limit(dev, oracle32, m):
+    d = 256
+    wg, wu, wd = W.weights(d, m, torch.bfloat16, layer=9)
+    layer, hw = device_layer(wg, wu, wd), host_f32(wg, wu, wd)
+    for k in (0.5, 0.9):
+        say("topk select limit m", m, "k", k)
+        _check(oracle32, layer, hw, _x(1, d, seed=m), k, f"m{m} B1 k{k}")
+
+
 @pytest.mark.parametrize("k", [0.3, 0.7])
 def test_topk_small_f32_residual(small_f32, oracle32, k):
     layer, hw = small_f32
