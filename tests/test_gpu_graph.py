@@ -91,9 +91,12 @@ def test_stack_graph(layers):
     _replay_check("stack", call, x_static, y_static, eager, _inputs(B, 1024, REPLAYS, 50))
 
 
-def test_topk_graph(layers):
+@pytest.mark.parametrize("B", [1, 2])
+def test_topk_graph(layers, B):
+    """One row selects inside the gate kernel (its ticket word: a replay
+    repeats the captured epoch and takes the compare-and-swap path), two
+    rows use the select kernel."""
     layer = layers[1]
-    B = 2
     x_static = torch.zeros((B, 1024), device="cuda")
     y_static = torch.empty_like(x_static)
     nb = int(P.raw().cats_topk_workspace_bytes(1024, 700, B))
