@@ -63,11 +63,11 @@ __device__ __forceinline__ void split8(const u32x4& a, const u32x4& b, bf16x8& h
 }
 
 // Weight steps a wave keeps in flight: a whole tile up to eight steps; at
-// ten (d = 5120) the x slice takes 80 registers and a whole tile 40 more,
-// past the 128 a wave has at four waves per SIMD, so the loads run two
-// steps ahead instead (five still spill).
+// ten (d = 5120) the x slice and a whole tile would take 120 of the 128
+// registers a wave has at four waves per SIMD, so the loads run five steps
+// ahead, with the lo fragments of steps 6..9 kept in LDS (XLR below).
 template <int KS>
-constexpr int gateup_window() { return KS <= 8 ? KS : 2; }
+constexpr int gateup_window() { return KS <= 8 ? KS : 5; }
 
 // KS: MFMA k-steps (32 columns each) per wave; the kernel covers
 // d = kGW * 32 * KS columns exactly, so no column needs a bounds check.
@@ -85,6 +85,10 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
   __shared__ int w_cnt[kGW + 1];
   __shared__ float l_ss[kGW][kBTileN];          // the waves' sums of squares per row
   __shared__ float l_scale[kBTileN];            // per-row factor on every dot product
+  // x-lo fragments of the steps from XLR on live in LDS, one slot per
+  // thread and step (read back by the same thread, so no barrier is needed)
+  constexpr int XLR = KS <= 8 ? KS : 6;
+  __shared__ bf16x8 l_xl[(KS - XLR) > 0 ? (KS - XLR) * kGThreads : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & (kWaveSize - 1);
@@ -143,6 +147,7 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       split8(wa[s % XWIN], wb[s % XWIN], xh[s], xl[s], ss);
+      if (s >= XLR) l_xl[(s - XLR) * kGThreads + tid] = xl[s];
       if (s + XWIN < KS) {
         wa[s % XWIN] = ld_buf16(rx, xrow + (s + XWIN) * 128u);
         wb[s % XWIN] = ld_buf16(rx, xrow + (s + XWIN) * 128u + 16u);
@@ -205,10 +210,10 @@ __global__ __launch_bounds__(kGThreads) void k_mlp_gateup_mfma(BatchedArgs a) {
       const bf16x8 av = as_bf16x8(buf[s % WIN]);
       if (s & 1) {
         ah1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, xh[s], ah1, 0, 0, 0);
-        al1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, xl[s], al1, 0, 0, 0);
+        al1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, s < XLR ? xl[s] : l_xl[(s - XLR) * kGThreads + tid], al1, 0, 0, 0);
       } else {
         ah0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, xh[s], ah0, 0, 0, 0);
-        al0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, xl[s], al0, 0, 0, 0);
+        al0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, s < XLR ? xl[s] : l_xl[(s - XLR) * kGThreads + tid], al0, 0, 0, 0);
       }
       if (s >= 1) buf[(s - 1) % WIN] = ld_ahead(s - 1 + WIN);
       __builtin_amdgcn_sched_barrier(0);
