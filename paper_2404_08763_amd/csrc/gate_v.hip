@@ -32,6 +32,7 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_gate_v(GateVArgs a) 
   __shared__ uint32_t l_mask[SEG ? kFusedMaxNeurons : 1];
   __shared__ int w_cnt[W + 1];
   __shared__ __attribute__((aligned(16))) uint32_t hist[SEL ? kSelHistBins : 1];
+  __shared__ float l_vs[SEL ? kFusedMaxNeurons : 1];  // the block's v, stored in one burst at the end
   __shared__ uint32_t s_state[4];
   __shared__ int s_last;
 
@@ -63,7 +64,7 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_gate_v(GateVArgs a) 
         const float v = silu(g[b]);
         if (lane == 0 && i < ni) {
           if constexpr (SEL)
-            __hip_atomic_store(a.v + j, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            l_vs[w + i * W] = v;
           else
             a.v[(size_t)b * m + j] = v;
         }
@@ -84,6 +85,10 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_gate_v(GateVArgs a) 
     if (tid == 0) a.seg_cnt[blockIdx.x] = cnt;
   }
   if constexpr (SEL) {
+    // the block's v as consecutive device-coherent stores (whole lines)
+    __syncthreads();
+    for (int q = tid; q < nr.nb; q += NT)
+      __hip_atomic_store(a.v + nr.n0 + q, l_vs[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __builtin_amdgcn_s_waitcnt(0);  // this thread's v stores have completed
     __syncthreads();
     if (tid == 0) {
