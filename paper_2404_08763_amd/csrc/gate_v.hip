@@ -12,12 +12,11 @@
 //
 // With SEL (one row, m up to kGateSelMaxM) the kernel also fixes the row's
 // top-k cutoff: every block writes its v with device-coherent stores and
-// takes a ticket (the sparse-input kernel's epoch-tagged count: one atomic
-// add when the word carries this call's tag, a compare-and-swap restart on
-// a stale one); the last block to arrive reads the whole row back and
-// selects its r-th smallest |v| (topk_select.hpp), so no separate select
-// launch is needed.  No block waits for another.
+// takes a ticket (ticket.hpp); the last block to arrive reads the whole row
+// back and selects its r-th smallest |v| (topk_select.hpp), so no separate
+// select launch is needed.  No block waits for another.
 #include "gemv_rows.hpp"
+#include "ticket.hpp"
 #include "topk_select.hpp"
 
 namespace cats {
@@ -37,6 +36,11 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_gate_v(GateVArgs a) 
   __shared__ int s_last;
 
   const int tid = threadIdx.x;
+  // (with SEL the ticket word is read now, so that arriving costs one atomic)
+  unsigned long long peek = 0ull;
+  if constexpr (SEL) {
+    if (tid == 0) peek = ticket_peek(a.ticket);
+  }
   const int lane = tid & (kWaveSize - 1);
   const int w = __builtin_amdgcn_readfirstlane(tid / kWaveSize);
   const int B = a.B, d = a.d, m = a.m;
@@ -91,25 +95,7 @@ __global__ __launch_bounds__(kFusedWaves* kWaveSize) void k_gate_v(GateVArgs a) 
       __hip_atomic_store(a.v + nr.n0 + q, l_vs[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __builtin_amdgcn_s_waitcnt(0);  // this thread's v stores have completed
     __syncthreads();
-    if (tid == 0) {
-      const unsigned long long tag = (unsigned long long)a.epoch << 32;
-      unsigned long long old = __hip_atomic_fetch_add(a.ticket, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      unsigned long long want = old + 1ull;
-      if ((old >> 32) != (unsigned long long)a.epoch) {
-        old = __hip_atomic_load(a.ticket, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        for (;;) {
-          want = ((old >> 32) == (unsigned long long)a.epoch) ? old + 1ull : (tag | 1ull);
-          if (__hip_atomic_compare_exchange_strong(a.ticket, &old, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                   __HIP_MEMORY_SCOPE_AGENT))
-            break;
-        }
-      }
-      s_last = (int)(want & 0xffffffffull) == (int)gridDim.x;
-      if (s_last) {
-        const uint32_t next = a.epoch == 0xffffffffu ? 1u : a.epoch + 1u;
-        __hip_atomic_store(a.ticket, (unsigned long long)next << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
+    if (tid == 0) s_last = take_ticket(a.ticket, a.epoch, gridDim.x, peek);
     __syncthreads();
     if (!s_last) return;
     // the last block: every block's v is in memory

@@ -14,17 +14,14 @@
 // for one group (NG = 1): y is written directly and consecutive column tiles
 // run on one XCD, so its L2 serves both halves of each 128-byte line.
 // Narrower outputs split the channels into NG > 1 groups: the blocks of a
-// column tile leave
-// device-coherent partial sums and take a ticket; the last of them adds the
-// NG partials in group order (deterministic), adds the residual and writes
-// y.  No block waits for another.  The ticket is a count in a word tagged
-// with the call's epoch: one atomic add when the word already carries this
-// call's tag, else a compare-and-swap that restarts the count under it, so
-// leftovers of earlier calls in the workspace never count (the swap loop
-// only repeats when another block's swap succeeded, at most NG times).  The
-// last block leaves the count at zero under the next epoch's tag.
+// column tile leave device-coherent partial sums and take a ticket; the
+// last of them adds the NG partials in group order (deterministic), adds
+// the residual and writes y.  No block waits for another: the ticket (ticket.hpp) is a count in a
+// word tagged with the call's epoch, so leftovers of earlier calls in the
+// workspace never count.
 #include "device.hpp"
 #include "internal.hpp"
+#include "ticket.hpp"
 
 namespace cats {
 
@@ -59,6 +56,8 @@ __global__ __launch_bounds__(kSThreads) void k_sparse_input(SparseInputArgs a) {
     ct = blockIdx.x % CT;
     q = blockIdx.x / CT;
   }
+  // (the ticket word is read now, so that arriving costs one atomic)
+  const unsigned long long peek = (NG > 1 && tid == 0) ? ticket_peek(a.tickets + ct) : 0ull;
   const int c0 = (int)(((int64_t)q * d) / NG), c1 = (int)(((int64_t)(q + 1) * d) / NG);
   // A wave load covers RPL rows of the block's columns: LPR consecutive
   // lanes per row, 8 columns (16 bytes) each.
@@ -241,37 +240,7 @@ __global__ __launch_bounds__(kSThreads) void k_sparse_input(SparseInputArgs a) {
   }
   __builtin_amdgcn_s_waitcnt(0);  // this thread's partial store has completed
   __syncthreads();
-  if (tid == 0) {
-    unsigned long long* tk = a.tickets + ct;
-    const unsigned long long tag = (unsigned long long)a.epoch << 32;
-    // Fast path: the word already carries this call's tag (the previous
-    // call on this workspace left it so), and one atomic add counts the
-    // block.  Otherwise the word is stale: compare-and-swap until this
-    // call's tag is installed or counted on (an add that landed on the
-    // stale word is overwritten by the install, so it is not counted).
-    unsigned long long old = __hip_atomic_fetch_add(tk, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    unsigned long long want = old + 1ull;
-    if ((old >> 32) != (unsigned long long)a.epoch) {
-      old = __hip_atomic_load(tk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      for (;;) {
-        want = ((old >> 32) == (unsigned long long)a.epoch) ? old + 1ull : (tag | 1ull);
-        if (__hip_atomic_compare_exchange_strong(tk, &old, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT))
-          break;
-      }
-    }
-    s_last = (int)(want & 0xffffffffull) == NG;
-    // The tile's count is complete: leave it at zero under the tag that
-    // the next call carries when it directly follows this one (epochs
-    // count up and skip 0), so that call takes the fast path.  Any other
-    // next call (another workspace's call in between, or a replayed graph,
-    // which repeats its captured epoch) finds a stale tag and takes the
-    // compare-and-swap path, which is also exact.
-    if (s_last) {
-      const uint32_t next = a.epoch == 0xffffffffu ? 1u : a.epoch + 1u;
-      __hip_atomic_store(tk, (unsigned long long)next << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
+  if (tid == 0) s_last = take_ticket(a.tickets + ct, a.epoch, (uint32_t)NG, peek);
   __syncthreads();
   if (!s_last || !item) return;
   // the last block of the tile: every group's partial, in group order
