@@ -621,8 +621,9 @@ def profile_set(P, W, torch, layers, xs, thr, ks, calls=6):
     run(f"forward with active lists B=1 k={k5}", ["k_mlp_fused (aux)", "k_mlp_reduce (sum and lists)"],
         lambda c: P.mlp_forward(layers[c % R], x1[c], t5, out=y1, aux=True), sw * d * (m + 2 * U1) + 8 * d + 16 * U1)
     kept = m - max(1, int(np.ceil(k5 * m - 1e-6))) + 1
+    wst = torch.zeros(int(P.raw().cats_topk_workspace_bytes(d, m, 1)), dtype=torch.uint8, device=dev)
     run(f"top-k B=1 k={k5}", ["k_gate_v (with the cutoff select)", "k_mlp_fused (given v)", "k_mlp_reduce"],
-        lambda c: P.mlp_forward_topk(layers[c % R], x1[c], k5, out=y1), sw * d * (m + 2 * kept) + 8 * d + 8 * m)
+        lambda c: P.mlp_forward_topk(layers[c % R], x1[c], k5, out=y1, ws=wst), sw * d * (m + 2 * kept) + 8 * d + 8 * m)
     for mode in ("mask", "index"):
         run(f"unfused {mode} B=1 k={k5}", ["k_gate_v", "k_unfused_up", "k_unfused_down", "k_mlp_reduce"],
             lambda c, mode=mode: P.mlp_forward_unfused(layers[c % R], x1[c], t5, mode=mode, out=y1),
