@@ -111,3 +111,32 @@ def test_sparse_input_deterministic(B):
     y2, a2 = P.sparse_input_gemv(w, x, 0.6, ws=_garbage_like(ws), aux=True)
     _same(y1, y2, f"sparse input B{B} y")
     _same_lists(a1, a2, B, f"sparse input B{B}")
+
+
+def test_tickets_alternating_workspaces(c2):
+    """The arrival tickets of the one-row top-k select and of the
+    sparse-input product with two workspaces used in turn, so that every
+    call finds its ticket words left by a call with another epoch (the
+    compare-and-swap install), against calls that always find their own tag:
+    the same bits on every call."""
+    c, layer = c2
+    x = W.decode_vectors(c, 6).cuda()
+    nb = int(P.raw().cats_topk_workspace_bytes(c.d, c.m, 1))
+    wa, wb, wone = (torch.zeros(nb, dtype=torch.uint8, device="cuda") for _ in range(3))
+    say("tickets: top-k, alternating workspaces")
+    for i in range(6):
+        xi = x[i : i + 1].contiguous()
+        y1, t1 = P.mlp_forward_topk(layer, xi, 0.7, ws=wone)
+        y2, t2 = P.mlp_forward_topk(layer, xi, 0.7, ws=wa if i % 2 else wb)
+        _same(y1, y2, f"top-k call {i} y")
+        _same(t1, t2, f"top-k call {i} t")
+    d, n = 4096, 1024
+    g = torch.Generator().manual_seed(77)
+    w = (torch.randn((d, n), generator=g) * 0.02).to(torch.bfloat16).cuda()
+    xs = torch.randn((6, d), generator=g).cuda()
+    sa, sb, sone = (P.sparse_input_workspace(d, n, 1) for _ in range(3))
+    say("tickets: sparse input, alternating workspaces")
+    for i in range(6):
+        xi = xs[i : i + 1].contiguous()
+        _same(P.sparse_input_gemv(w, xi, 0.6, ws=sone), P.sparse_input_gemv(w, xi, 0.6, ws=sa if i % 2 else sb),
+              f"sparse input call {i}")
