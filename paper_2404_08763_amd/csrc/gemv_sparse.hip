@@ -21,6 +21,7 @@
 // workspace never count.
 #include "device.hpp"
 #include "internal.hpp"
+#include "scan.hpp"
 #include "ticket.hpp"
 
 namespace cats {
@@ -100,12 +101,7 @@ __global__ __launch_bounds__(kSThreads) void k_sparse_input(SparseInputArgs a) {
         if (bq < B && cl0 + u < nc && !(fabsf(xv[u][bq]) < a.t)) mk[u] |= 1u << bq;
       mine += mk[u] != 0u;
     }
-    int incl = mine;  // inclusive scan over the wave's lanes
-#pragma unroll
-    for (int o = 1; o < kWaveSize; o <<= 1) {
-      const int v = __shfl_up(incl, o);
-      if (lane >= o) incl += v;
-    }
+    const int incl = (int)wave_incl_scan((uint32_t)mine);  // inclusive scan over the wave's lanes
     if (lane == kWaveSize - 1) w_tot[w] = incl;
     __syncthreads();
     int pos = incl - mine;

@@ -4,6 +4,7 @@
 // list (the compressed index list of the Appendix D kernel algorithm).
 #include "device.hpp"
 #include "internal.hpp"
+#include "scan.hpp"
 
 namespace cats {
 
@@ -157,12 +158,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
     __syncthreads();
     if (w == 0) {  // exclusive scan of the 64 counts, entry order = (k, w)
       const int c = s_off[lane];
-      int incl = c;
-#pragma unroll
-      for (int o = 1; o < kWaveSize; o <<= 1) {
-        const int v = __shfl_up(incl, o);
-        if (lane >= o) incl += v;
-      }
+      const int incl = (int)wave_incl_scan((uint32_t)c);
       s_off[lane] = incl - c;
       if (lane == kWaveSize - 1) s_off[kFinCounts] = incl;
     }

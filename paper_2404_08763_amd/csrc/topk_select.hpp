@@ -7,10 +7,12 @@
 // digits fixed so far; the bin holding the remaining rank becomes the next
 // digit.  The row's keys stay in registers across the passes (KPT per
 // thread of the NT-thread block; padding keys have bit 31 set and never
-// match), and one wave finds the bin by a prefix sum over its lanes.
+// match), and one wave finds the bin by a prefix sum over its lanes (DPP,
+// scan.hpp).
 #pragma once
 
 #include "device.hpp"
+#include "scan.hpp"
 
 namespace cats {
 
@@ -41,12 +43,7 @@ __device__ __forceinline__ void select_pass(const uint32_t (&key)[KPT], uint32_t
       h[q + 3] = v.w;
       sum += v.x + v.y + v.z + v.w;
     }
-    uint32_t incl = sum;
-#pragma unroll
-    for (int o = 1; o < kWaveSize; o <<= 1) {
-      const uint32_t u = (uint32_t)__shfl_up((int)incl, o);
-      if (tid >= o) incl += u;
-    }
+    const uint32_t incl = wave_incl_scan(sum);
     // lowest lane whose running count reaches the rank (one exists: the
     // matching keys number at least rem)
     const uint64_t hit = __ballot(incl >= (uint32_t)rem);
