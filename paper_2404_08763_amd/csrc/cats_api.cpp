@@ -3,12 +3,14 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
+#include <random>
 #include <string>
 #include <vector>
 
@@ -647,9 +649,24 @@ GemvLayout gemv_layout(int d, int n, int B) {
   return L;
 }
 
-// Tags of successive sparse-input calls (never 0), so a column tile's
-// ticket word left by any earlier call is recognised as stale.
-std::atomic<uint32_t> g_epoch{0};
+// Tags of successive ticketed calls (sparse input, the top-k select; never
+// 0), so a ticket word left by any earlier call is recognised as stale.  The
+// sequence starts at a random point of the 32-bit range, not at 1: a
+// workspace shared between entry points can leave data in a ticket word,
+// and data is full of small integers (indices, counts), which a counter
+// starting at 1 would meet within its first thousands of calls.
+uint32_t epoch_start() {
+  uint32_t s = 0x9e3779b9u;
+  try {
+    std::random_device rd;
+    s ^= rd();
+  } catch (...) {
+  }
+  s ^= (uint32_t)std::chrono::steady_clock::now().time_since_epoch().count();
+  s ^= (uint32_t)(reinterpret_cast<uintptr_t>(&s) >> 4);
+  return s;
+}
+std::atomic<uint32_t> g_epoch{epoch_start()};
 uint32_t next_epoch() {
   uint32_t e;
   do {
