@@ -36,7 +36,9 @@
  *  - Scratch memory comes from a caller-provided workspace `ws` of
  *    `ws_bytes` bytes (256-byte aligned, device), sized with
  *    cats_workspace_bytes().  Calls that run concurrently need separate
- *    workspaces.
+ *    workspaces.  A workspace needs no clearing: it may hold anything when
+ *    a call starts (leftovers of other calls or entry points included);
+ *    the arrival counters some kernels keep there are tagged per call.
  *  - x, y, residual, thresholds and calibration inputs are fp32.  Weights
  *    are CATS_F32 or CATS_BF16; all arithmetic accumulates in fp32.
  *  - Weight layout is neuron-major: W_gate^T and W_up^T are stored [m x d]
