@@ -124,9 +124,8 @@ __global__ __launch_bounds__(kReduceThreads) void k_mlp_reduce(ReduceArgs a) {
         cnt += (p < p_lo && listed(mk[k])) ? 1 : 0;
       }
     }
-#pragma unroll
-    for (int o = kWaveSize / 2; o >= 1; o >>= 1) cnt += __shfl_xor(cnt, o);
-    if (lane == 0) s_off[w] = cnt;
+    const int wcnt = (int)wave_incl_scan((uint32_t)cnt);  // the last lane holds the wave's count
+    if (lane == kWaveSize - 1) s_off[w] = wcnt;
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < kReduceWaves; ++k) run += s_off[k];
